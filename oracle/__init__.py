@@ -1,0 +1,105 @@
+"""fp64 CPU oracle for scaled-dot-product attention forward.
+
+TEST INFRASTRUCTURE.  Only the test suite, the smoke check and the bench's
+CPU-baseline leg may import this package.  The product path (the HIP library
+and its binding) never imports or calls it, and it imports nothing from the
+product: inputs arrive as bfloat16 bit arrays from the seeded generator.
+
+The arithmetic lives in ``attn_oracle.c``: the plain softmax-attention
+definition, row by row, in double precision (bottom-right causal alignment,
+grouped-query head map h -> h // (Hq/Hkv), LSE as a natural log).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+_lib = None
+_i64 = ctypes.c_int64
+_ptr = ctypes.c_void_p
+
+
+def load(path: str | None = None):
+    """Load (building first if absent) the oracle library; returns the handle."""
+    global _lib
+    if path is None and _lib is not None:
+        return _lib
+    lib_path = path or _build.LIB
+    if not os.path.exists(lib_path):
+        _build.build()
+    lib = ctypes.CDLL(lib_path)
+    lib.oracle_attn_fwd.restype = ctypes.c_int
+    lib.oracle_attn_fwd.argtypes = [_ptr, _ptr, _ptr, _ptr, _ptr, _i64, _i64, _i64, _i64,
+                                    _i64, _i64, ctypes.c_int, ctypes.c_double, ctypes.c_int]
+    lib.oracle_attn_rows.restype = ctypes.c_int
+    lib.oracle_attn_rows.argtypes = [_ptr, _ptr, _ptr, _i64, _i64, _i64, _i64, _i64, _i64,
+                                     ctypes.c_int, ctypes.c_double, _ptr, _i64, _ptr, _ptr,
+                                     ctypes.c_int]
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def default_threads() -> int:
+    """Host threads for the oracle: the cores this process may run on,
+    capped at 16 (a GPU machine's CPU share)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _bits(a) -> np.ndarray:
+    a = np.ascontiguousarray(a)
+    if a.dtype != np.uint16 or a.ndim != 4:
+        raise TypeError("oracle inputs are 4-D bfloat16 bit arrays (numpy.uint16, BHSD)")
+    return a
+
+
+def _shape(q, k, v):
+    B, Hq, Sq, D = q.shape
+    Bk, Hkv, Sk, Dk = k.shape
+    if (Bk, Dk) != (B, D) or v.shape != k.shape:
+        raise OracleError(f"inconsistent shapes q{q.shape} k{k.shape} v{v.shape}")
+    return B, Hq, Hkv, Sq, Sk, D
+
+
+def attn_fwd(q, k, v, causal: bool, scale: float, nthreads: int | None = None, lib=None):
+    """Every output row: returns (O [B,Hq,Sq,D], LSE [B,Hq,Sq]) as float64."""
+    q, k, v = _bits(q), _bits(k), _bits(v)
+    B, Hq, Hkv, Sq, Sk, D = _shape(q, k, v)
+    o = np.empty((B, Hq, Sq, D), dtype=np.float64)
+    lse = np.empty((B, Hq, Sq), dtype=np.float64)
+    lib = lib or load()
+    rc = lib.oracle_attn_fwd(q.ctypes.data, k.ctypes.data, v.ctypes.data, o.ctypes.data,
+                             lse.ctypes.data, B, Hq, Hkv, Sq, Sk, D, int(bool(causal)),
+                             float(scale), nthreads or default_threads())
+    if rc:
+        raise OracleError(f"oracle_attn_fwd returned {rc}")
+    return o, lse
+
+
+def attn_rows(q, k, v, causal: bool, scale: float, rows, nthreads: int | None = None, lib=None):
+    """Selected rows ``rows`` = [(b, h, i), ...]: returns (O [n,D], LSE [n])."""
+    q, k, v = _bits(q), _bits(k), _bits(v)
+    B, Hq, Hkv, Sq, Sk, D = _shape(q, k, v)
+    idx = np.ascontiguousarray(np.asarray(rows, dtype=np.int64).reshape(-1, 3))
+    n = idx.shape[0]
+    o = np.empty((n, D), dtype=np.float64)
+    lse = np.empty((n,), dtype=np.float64)
+    lib = lib or load()
+    rc = lib.oracle_attn_rows(q.ctypes.data, k.ctypes.data, v.ctypes.data, B, Hq, Hkv, Sq, Sk,
+                              D, int(bool(causal)), float(scale), idx.ctypes.data, n,
+                              o.ctypes.data, lse.ctypes.data, nthreads or default_threads())
+    if rc:
+        raise OracleError(f"oracle_attn_rows returned {rc}")
+    return o, lse

@@ -1,0 +1,145 @@
+"""Seeded synthetic inputs for attention forward: the one module that both the
+HIP path (through the tests and the bench) and the CPU oracle consume.
+
+It holds none of attention's arithmetic: it draws i.i.d. normal samples,
+rounds them to bfloat16 and applies the input recipe of each workload.  Every
+tensor is returned as raw bfloat16 bit patterns (``numpy.uint16``) in the
+contiguous BHSD layout ``[batch, heads, seq, head_dim]``.
+
+Random numbers come from numpy's counter-based Philox-4x32-10 generator
+(Salmon et al., SC'11).  Each tensor has its own substream, keyed by
+``(seed, workload id, tensor id)``, so any tensor can be regenerated alone and
+two tensors never share draws.
+"""
+from __future__ import annotations
+
+import dataclasses
+import hashlib
+import math
+
+import numpy as np
+
+TENSOR_Q, TENSOR_K, TENSOR_V = 0, 1, 2
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    """One attention-forward problem: shapes, masking and input recipe."""
+
+    name: str
+    wid: int          # substream id of the workload
+    B: int
+    Hq: int
+    Hkv: int
+    Sq: int
+    Sk: int
+    D: int
+    causal: bool
+    peaky_every: int = 0      # 0: no peaky rows; else scale key rows j % peaky_every == 0
+    peaky_factor: float = 1.0  # ... by this power of two
+
+    @property
+    def scale(self) -> float:
+        """Softmax scale 1/sqrt(D), rounded to the fp32 value both sides use."""
+        return float(np.float32(1.0 / math.sqrt(self.D)))
+
+    def pairs(self) -> int:
+        """Number of visible (query, key) pairs in one head."""
+        if not self.causal:
+            return self.Sq * self.Sk
+        off = self.Sk - self.Sq
+        return sum(min(self.Sk, i + 1 + off) for i in range(self.Sq))
+
+    def flops(self) -> int:
+        """Matmul flops of the forward pass over visible pairs only: QK^T and
+        PV each cost 2*D flops per visible pair."""
+        return 4 * self.D * self.B * self.Hq * self.pairs()
+
+    def bytes(self) -> int:
+        """Algorithmic HBM bytes: bf16 Q, K, V read once, fp32 O and LSE
+        written once."""
+        q = self.B * self.Hq * self.Sq * self.D
+        kv = self.B * self.Hkv * self.Sk * self.D
+        return 2 * (q + 2 * kv) + 4 * q + 4 * self.B * self.Hq * self.Sq
+
+    def describe(self) -> str:
+        s = (f"B={self.B} Hq={self.Hq} Hkv={self.Hkv} Sq={self.Sq} Sk={self.Sk} "
+             f"D={self.D} {'causal' if self.causal else 'non-causal'}")
+        if self.peaky_every:
+            s += f", key rows j%{self.peaky_every}==0 x{self.peaky_factor:g}"
+        return s
+
+
+# The five workloads: a tiny correctness case, a causal D=64 case, the dense
+# D=128 throughput case, a long causal case with peaky keys and a grouped-query
+# causal case.  All draw Q/K/V i.i.d. N(0,1) in bf16 with scale 1/sqrt(D).
+WORKLOADS = {
+    w.name: w
+    for w in (
+        Workload("tiny_d64_s128", 0, 1, 2, 2, 128, 128, 64, False),
+        Workload("causal_d64_s1k", 1, 4, 16, 16, 1024, 1024, 64, True),
+        Workload("dense_d128_s2k", 2, 8, 32, 32, 2048, 2048, 128, False),
+        Workload("causal_peaky_d128_s8k", 3, 1, 32, 32, 8192, 8192, 128, True,
+                 peaky_every=64, peaky_factor=8.0),
+        Workload("gqa4_causal_d128_s4k", 4, 2, 32, 8, 4096, 4096, 128, True),
+    )
+}
+
+
+def bf16_from_f32(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bfloat16 with round-to-nearest-even and return
+    the bit patterns.  Inputs here are finite, so no NaN special case."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    bias = np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
+    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+
+
+def f32_from_bf16(u: np.ndarray) -> np.ndarray:
+    """Widen bfloat16 bit patterns to float32 (exact)."""
+    return (np.asarray(u, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _stream(seed: int, wid: int, tensor: int) -> np.random.Generator:
+    key = np.array([seed & 0xFFFFFFFFFFFFFFFF, (wid << 8) | tensor], dtype=np.uint64)
+    return np.random.Generator(np.random.Philox(key=key))
+
+
+def normal_bf16(shape, seed: int, wid: int, tensor: int) -> np.ndarray:
+    """i.i.d. N(0,1) samples of the given shape, as bfloat16 bits."""
+    g = _stream(seed, wid, tensor)
+    x = g.standard_normal(size=int(np.prod(shape)), dtype=np.float32)
+    return bf16_from_f32(x).reshape(shape)
+
+
+def scale_rows_bf16(u: np.ndarray, every: int, factor: float) -> np.ndarray:
+    """Multiply rows j % every == 0 (axis -2) by ``factor``.  For a power of
+    two this is exact in bfloat16 for the normal samples drawn here."""
+    out = u.copy()
+    rows = f32_from_bf16(out[..., ::every, :]) * np.float32(factor)
+    out[..., ::every, :] = bf16_from_f32(rows)
+    return out
+
+
+def make_inputs(w: Workload, seed: int = 0):
+    """(q, k, v) bfloat16 bit arrays for workload ``w``."""
+    q = normal_bf16((w.B, w.Hq, w.Sq, w.D), seed, w.wid, TENSOR_Q)
+    k = normal_bf16((w.B, w.Hkv, w.Sk, w.D), seed, w.wid, TENSOR_K)
+    v = normal_bf16((w.B, w.Hkv, w.Sk, w.D), seed, w.wid, TENSOR_V)
+    if w.peaky_every:
+        k = scale_rows_bf16(k, w.peaky_every, w.peaky_factor)
+    return q, k, v
+
+
+def random_problem(B, Hq, Hkv, Sq, Sk, D, seed: int, wid: int = 100, std: float = 1.0):
+    """(q, k, v) bfloat16 bits for an ad-hoc shape (tests' edge cases)."""
+    def one(shape, t):
+        g = _stream(seed, wid, t)
+        x = g.standard_normal(size=int(np.prod(shape)), dtype=np.float32) * np.float32(std)
+        return bf16_from_f32(x).reshape(shape)
+    return (one((B, Hq, Sq, D), TENSOR_Q), one((B, Hkv, Sk, D), TENSOR_K),
+            one((B, Hkv, Sk, D), TENSOR_V))
+
+
+def digest(u: np.ndarray) -> str:
+    """Short BLAKE2b digest of an array's bytes (records which inputs ran)."""
+    return hashlib.blake2b(np.ascontiguousarray(u).view(np.uint8), digest_size=8).hexdigest()
