@@ -1,0 +1,205 @@
+"""Benchmark of the fused attention forward (libtileattn) on one MI355X.
+
+A step is one attn_fwd launch over one batch of the workload, inputs already
+resident in HBM.  Prints ONE JSON line with the throughput in TFLOP/s (matmul
+flops over visible query-key pairs), the roofline position of the kernel
+against the dense bf16 MFMA peak, and the fp64 CPU oracle's throughput on a
+bounded sample of the same workload as a reported baseline.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+  python bench.py --copy-probe      # plain device copy of known size, for
+                                    # scaling rocprofv3 FETCH_SIZE/WRITE_SIZE
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2504_17577_amd import gen  # noqa: E402
+
+METRIC = "attention fwd TFLOP/s and % of MI355X bf16 MFMA peak, 1 GPU"
+DEFAULT_WORKLOAD = "dense_d128_s2k"
+# MI355X dense bf16 MFMA peak: 256 CUs x 2.4 GHz x 4096 flop/clk/CU
+PEAK_BF16_TFLOPS = 2516.6
+HBM_PEAK_GBS = 8000.0
+KERNEL_SRC = os.path.join(ROOT, "paper_2504_17577_amd", "csrc", "attn_fwd.hip")
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def kernel_digest() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.blake2b(f.read(), digest_size=8).hexdigest()
+
+
+def read_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary, or
+    None when there is none or the kernel source changed since."""
+    path = os.path.join(PROFILES, f"attn_fwd_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_src = re.search(r"kernel_source_blake2b:\s*([0-9a-f]+)", text)
+    m_tr = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_src or not m_tr or m_src.group(1) != kernel_digest():
+        return None
+    return float(m_tr.group(1))
+
+
+def to_device(a, torch):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def cpu_baseline(w, q, k, v, budget_s: float = 15.0):
+    """fp64 oracle throughput on whole heads of the workload, as many as fit
+    in about ``budget_s`` seconds of wall time (at least one)."""
+    import oracle
+
+    threads = oracle.default_threads()
+    lib = oracle.load()
+
+    def head_rows(hidx):
+        b, h = divmod(hidx, w.Hq)
+        i = np.arange(w.Sq, dtype=np.int64)
+        return np.stack([np.full_like(i, b), np.full_like(i, h), i], axis=1)
+
+    t0 = time.perf_counter()
+    oracle.attn_rows(q, k, v, w.causal, w.scale, head_rows(0), nthreads=threads, lib=lib)
+    t1 = time.perf_counter() - t0
+    n_heads = int(max(1, min(w.B * w.Hq - 1, budget_s / max(t1, 1e-6) - 1)))
+    rows = np.concatenate([head_rows(1 + i) for i in range(n_heads)]) if n_heads else None
+    t0 = time.perf_counter()
+    oracle.attn_rows(q, k, v, w.causal, w.scale, rows, nthreads=threads, lib=lib)
+    dt = time.perf_counter() - t0
+    flops = w.flops() / (w.B * w.Hq) * n_heads
+    return {
+        "value": flops / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{n_heads} of {w.B * w.Hq} heads of {w.name} (all {w.Sq} query rows each), "
+                  f"fp64 C oracle, {dt:.1f} s wall",
+    }
+
+
+def copy_probe(torch, mib: int = 1024, reps: int = 5):
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4,
+                      "reps": reps}), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(gen.WORKLOADS))
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the attention forward here has no multi-GPU "
+              f"path (asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2504_17577_amd import tileattn
+
+    if args.copy_probe:
+        copy_probe(torch)
+        return
+
+    w = gen.WORKLOADS[args.workload]
+    q, k, v = gen.make_inputs(w, seed=args.seed)
+    dq, dk, dv = to_device(q, torch), to_device(k, torch), to_device(v, torch)
+    o = torch.empty((w.B, w.Hq, w.Sq, w.D), dtype=torch.float32, device="cuda")
+    lse = torch.empty((w.B, w.Hq, w.Sq), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        tileattn.attn_fwd(dq, dk, dv, causal=w.causal, scale=w.scale, out=o, lse=lse,
+                          stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # spot check a few rows against the oracle so a broken build cannot post a number
+    import oracle
+    rows = [(0, 0, 0), (w.B - 1, w.Hq - 1, w.Sq - 1), (w.B // 2, w.Hq // 2, w.Sq // 2)]
+    ro, rl = oracle.attn_rows(q, k, v, w.causal, w.scale, rows)
+    idx = tuple(torch.tensor(c) for c in zip(*rows))
+    err_o = float(np.abs(o[idx].cpu().numpy() - ro).max())
+    err_l = float(np.abs(lse[idx].cpu().numpy() - rl).max())
+    if not (err_o <= 2e-2 and err_l <= 1e-3):
+        raise SystemExit(f"bench: result check failed (max|dO|={err_o}, max|dLSE|={err_l})")
+
+    # timed region: K launches on this stream between two HIP events
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = start.elapsed_time(end) / args.steps
+    tflops = w.flops() / (ms * 1e-3) / 1e12
+
+    traffic = read_traffic(w.name)
+    result = {
+        "metric": METRIC,
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "shape": w.describe(), "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv,
+                   "Sq": w.Sq, "Sk": w.Sk, "D": w.D, "causal": w.causal, "seed": args.seed,
+                   "flops_per_step": w.flops(), "inputs_blake2b": gen.digest(q)[:8] +
+                   gen.digest(k)[:8] + gen.digest(v)[:8]},
+        "pct_of_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(tflops, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+            "hbm_gbs_algorithmic": round(w.bytes() / (ms * 1e-3) / 1e9, 1),
+        },
+        "wall_s_timed": round(wall, 4),
+        "check": {"max_abs_dO": err_o, "max_abs_dLSE": err_l, "rows": len(rows)},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, q, k, v)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,100 @@
+/*
+ * tileattn — fused scaled-dot-product attention forward for AMD MI355X
+ * (gfx950), as a C ABI.
+ *
+ * The operation is the tile-fused attention kernel of the TileLang paper
+ * (arXiv 2504.17577): scores S = scale * Q K^T, a softmax over keys computed
+ * online over key tiles (running row max, rescale of the partial sums by the
+ * exponential of the max difference, running row sum, final division), and
+ * O = softmax(S) V, without ever storing S in memory.  The paper prints this
+ * recurrence in its appendix listing "Implementation of FlashMLA with
+ * TileLang" and benchmarks the multi-head forward in its FlashAttention
+ * experiment (Section "Numerical Experiments", table "FlashAttention shapes
+ * in our benchmark": batch, heads, sequence length, head dim 128, causal).
+ *
+ * Conventions for every entry point below:
+ *   - Layouts are contiguous row-major BHSD: Q and O are [B, Hq, Sq, D],
+ *     K and V are [B, Hkv, Sk, D], LSE is [B, Hq, Sq].  There are no stride
+ *     arguments.
+ *   - The caller owns every buffer.  The library allocates nothing, frees
+ *     nothing and keeps no state between calls; calls are thread-safe.
+ *   - Calls are asynchronous: they validate, enqueue on `stream` and return.
+ *     `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *   - All validation happens before any HIP call: a status other than TA_OK
+ *     means nothing was enqueued and no HIP API was touched (except for
+ *     TA_ERR_LAUNCH, reported by the HIP runtime after the launch).
+ *   - O and LSE are fully overwritten, never accumulated into.
+ */
+#ifndef TILEATTN_H
+#define TILEATTN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TA_OK = 0,
+    TA_ERR_NULL_POINTER = 1,  /* a required pointer is NULL                                 */
+    TA_ERR_INVALID_SHAPE = 2, /* a size < 1, Hq % Hkv != 0, causal with Sq > Sk, or an
+                                 element count beyond 2^31 per (batch, head) slice         */
+    TA_ERR_UNSUPPORTED = 3,   /* D is not 64 or 128                                         */
+    TA_ERR_MISALIGNED = 4,    /* a pointer is not 16-byte aligned                           */
+    TA_ERR_INVALID_SCALE = 5, /* scale is negative, NaN or infinite                         */
+    TA_ERR_ALIASING = 6,      /* O or LSE overlaps an input or each other                   */
+    TA_ERR_LAUNCH = 7         /* the HIP runtime reported an error for the launch           */
+} ta_status;
+
+/*
+ * attn_fwd — O = softmax(scale * Q K^T [+ causal mask]) V and its row
+ * log-sum-exp, for bf16 inputs with fp32 accumulation.
+ *
+ *   Q    device, bf16 [B, Hq, Sq, D]           read only
+ *   K    device, bf16 [B, Hkv, Sk, D]          read only
+ *   V    device, bf16 [B, Hkv, Sk, D]          read only
+ *   O    device, fp32 [B, Hq, Sq, D]           written
+ *   LSE  device, fp32 [B, Hq, Sq]              written: natural log of
+ *        sum_j exp(scale * q_i . k_j) over the keys row i may see
+ *   Hq % Hkv == 0; query head h reads key/value head h / (Hq / Hkv)
+ *   causal != 0: key j is visible to query i iff j <= i + (Sk - Sq)
+ *        (bottom-right alignment; requires Sq <= Sk so every row sees a key)
+ *   scale >= 0, finite; the kernel works in base 2 internally
+ *   D in {64, 128}; every pointer 16-byte aligned
+ *   stream: hipStream_t as void*
+ *
+ * The scores are formed in fp32 from bf16 products; the softmax weights are
+ * rounded to bf16 (round to nearest even) before the P V product.
+ */
+ta_status attn_fwd(const void *Q, const void *K, const void *V, float *O, float *LSE,
+                   int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, float scale,
+                   void *stream);
+
+/*
+ * ta_schedule — host-side tile schedule of attn_fwd, for tests and tools.
+ * For the query tile `q_tile` (rows q_tile*BM .. q_tile*BM+BM-1, BM from
+ * ta_tile_shape) it reports how many key tiles of BN keys the kernel visits
+ * (n_kv_tiles; tiles past it are skipped because every key in them is
+ * masked) and the first visited tile that needs per-element masking
+ * (first_masked; == n_kv_tiles if none).  Pure integer logic, no HIP call.
+ * Returns TA_ERR_INVALID_SHAPE for sizes < 1, q_tile out of range, or causal
+ * with Sq > Sk; TA_ERR_UNSUPPORTED for D not 64/128; TA_ERR_NULL_POINTER.
+ */
+ta_status ta_schedule(int Sq, int Sk, int D, int causal, int q_tile,
+                      int *n_kv_tiles, int *first_masked);
+
+/* Query rows (BM) and keys (BN) per tile for head dim D; TA_ERR_UNSUPPORTED
+ * for D not 64/128.  No HIP call. */
+ta_status ta_tile_shape(int D, int *BM, int *BN);
+
+/* Static text for a status code (never NULL). */
+const char *ta_status_string(ta_status s);
+
+/* Library version, major*10000 + minor*100 + patch. */
+int ta_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TILEATTN_H */

@@ -1,0 +1,216 @@
+"""GPU parity: libtileattn against the fp64 CPU oracle on the same seeded bf16
+inputs, through the C ABI (the Python binding only marshals pointers).
+
+Tolerances are the ones the attention-forward target states for bf16 inputs:
+max |O - O_ref| <= 2e-2 and max |LSE - LSE_ref| <= 1e-3 (absolute, every
+compared element).  Outputs are pre-filled with NaN so that any element the
+kernel fails to write fails the comparison.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2504_17577_amd import gen
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+O_TOL, LSE_TOL = 2e-2, 1e-3
+
+
+@pytest.fixture(scope="module")
+def ta():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2504_17577_amd import tileattn
+    tileattn.lib()
+    return tileattn
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def run(ta, q, k, v, causal, scale, stream=None):
+    B, Hq, Sq, D = q.shape
+    o = torch.full((B, Hq, Sq, D), float("nan"), dtype=torch.float32, device="cuda")
+    lse = torch.full((B, Hq, Sq), float("nan"), dtype=torch.float32, device="cuda")
+    dq, dk, dv = dev(q), dev(k), dev(v)   # held until the launch has finished
+    ta.attn_fwd(dq, dk, dv, causal=causal, scale=scale, out=o, lse=lse, stream=stream)
+    torch.cuda.synchronize()
+    return o, lse
+
+
+def report(tag, eo, el):
+    print(f"{tag}: max|dO|={eo:.3e} max|dLSE|={el:.3e}", flush=True)
+
+
+def compare_full(ta, q, k, v, causal, scale, tag):
+    o, lse = run(ta, q, k, v, causal, scale)
+    ro, rl = oracle.attn_fwd(q, k, v, causal, scale)
+    o, lse = o.cpu().numpy(), lse.cpu().numpy()
+    assert np.isfinite(o).all() and np.isfinite(lse).all(), f"{tag}: unwritten or non-finite output"
+    eo, el = float(np.abs(o - ro).max()), float(np.abs(lse - rl).max())
+    report(tag, eo, el)
+    assert eo <= O_TOL and el <= LSE_TOL, tag
+    return o, lse
+
+
+@pytest.mark.parametrize("name", ["tiny_d64_s128", "causal_d64_s1k"])
+def test_workload_full_compare(ta, name):
+    w = gen.WORKLOADS[name]
+    q, k, v = gen.make_inputs(w, seed=0)
+    compare_full(ta, q, k, v, w.causal, w.scale, name)
+
+
+def sample_rows(w, rng, n_random):
+    """Rows to check at full size: tile edges, first/last rows, random rows."""
+    rows = set()
+    heads = [(0, 0), (w.B - 1, w.Hq - 1), (w.B // 2, w.Hq // 2)]
+    for b, h in heads:
+        for i in (0, 1, 31, 32, 63, 64, 127, 128, w.Sq // 2, w.Sq - 129, w.Sq - 2, w.Sq - 1):
+            if 0 <= i < w.Sq:
+                rows.add((b, h, i))
+    for _ in range(n_random):
+        rows.add((int(rng.integers(w.B)), int(rng.integers(w.Hq)), int(rng.integers(w.Sq))))
+    return sorted(rows)
+
+
+@pytest.mark.parametrize("name", ["dense_d128_s2k", "causal_peaky_d128_s8k", "gqa4_causal_d128_s4k"])
+def test_workload_full_size_sampled(ta, name):
+    """Full-size workload, in the launch configuration the bench times:
+    sampled rows against the oracle, plus properties over every row."""
+    w = gen.WORKLOADS[name]
+    q, k, v = gen.make_inputs(w, seed=0)
+    o, lse = run(ta, q, k, v, w.causal, w.scale)
+    # every element written and finite
+    assert bool(torch.isfinite(o).all()) and bool(torch.isfinite(lse).all()), name
+    # each O row is a weighted mean of V rows.  The kernel rounds the weights
+    # to bf16 (relative error <= 2^-8 each) and divides by the fp32 sum, so
+    # the weights sum to 1 within 2^-8: O lies in [min V, max V] widened by
+    # 2^-7 * max|V| per column.
+    g = w.Hq // w.Hkv
+    vf = torch.from_numpy(gen.f32_from_bf16(v)).cuda()
+    vmin = vf.amin(dim=2).repeat_interleave(g, 1)[:, :, None, :]
+    vmax = vf.amax(dim=2).repeat_interleave(g, 1)[:, :, None, :]
+    margin = 2.0 ** -7 * torch.maximum(vmin.abs(), vmax.abs())
+    over = torch.maximum(o - (vmax + margin), (vmin - margin) - o).amax().item()
+    assert over <= 0, f"{name}: O outside the widened hull of V by {over:.3g}"
+    rows = sample_rows(w, np.random.default_rng(1), 512)
+    ro, rl = oracle.attn_rows(q, k, v, w.causal, w.scale, rows)
+    idx = tuple(torch.tensor(c) for c in zip(*rows))
+    go = o[idx].cpu().numpy()
+    gl = lse[idx].cpu().numpy()
+    eo, el = float(np.abs(go - ro).max()), float(np.abs(gl - rl).max())
+    report(f"{name} ({len(rows)} sampled rows)", eo, el)
+    assert eo <= O_TOL and el <= LSE_TOL, name
+
+
+EDGE = [
+    # (B, Hq, Hkv, Sq, Sk, D, causal)
+    (1, 1, 1, 1, 1, 64, False), (1, 1, 1, 1, 1, 128, True),
+    (1, 2, 2, 37, 37, 64, True), (1, 2, 1, 37, 37, 128, False),
+    (2, 4, 2, 129, 129, 64, True), (1, 2, 2, 129, 200, 128, True),
+    (1, 8, 1, 200, 1000, 128, True), (1, 8, 8, 1000, 1000, 64, False),
+    (1, 4, 4, 1, 1000, 128, True), (1, 4, 4, 1000, 37, 128, False),
+    (2, 6, 3, 65, 63, 64, False), (1, 16, 2, 300, 300, 128, True),
+    (1, 2, 2, 128, 129, 64, True), (1, 2, 2, 256, 256, 128, False),
+]
+
+
+@pytest.mark.parametrize("shape", EDGE, ids=[str(s) for s in EDGE])
+def test_edge_shapes(ta, shape):
+    B, Hq, Hkv, Sq, Sk, D, causal = shape
+    q, k, v = gen.random_problem(B, Hq, Hkv, Sq, Sk, D, seed=sum(shape))
+    compare_full(ta, q, k, v, causal, 1.0 / math.sqrt(D), str(shape))
+
+
+def test_causal_row0_is_v0(ta):
+    """Query 0 sees key 0 only.  Its weight is exp2 of the rounding residual of
+    the max score (about 1 +- 2^-22) and rounds to exactly 1.0 in bf16, while
+    the fp32 row sum keeps the residual: O = V[0] up to a few fp32 ulps."""
+    q, k, v = gen.random_problem(2, 4, 2, 300, 300, 128, seed=3)
+    o, lse = run(ta, q, k, v, True, 1 / math.sqrt(128))
+    vf = gen.f32_from_bf16(v)
+    o = o.cpu().numpy()
+    for h in range(4):
+        ref = vf[:, h // 2, 0, :]
+        assert np.all(np.abs(o[:, h, 0, :] - ref) <= 2.0 ** -20 * np.abs(ref))
+    ro, rl = oracle.attn_rows(q, k, v, True, 1 / math.sqrt(128), [(0, 0, 0), (1, 3, 0)])
+    assert abs(lse[0, 0, 0].item() - rl[0]) <= 1e-5 and abs(lse[1, 3, 0].item() - rl[1]) <= 1e-5
+
+
+def test_single_key(ta):
+    q, k, v = gen.random_problem(1, 2, 2, 130, 1, 64, seed=4)
+    o, _ = run(ta, q, k, v, False, 0.125)
+    ref = np.broadcast_to(gen.f32_from_bf16(v)[:, :, :1, :], o.shape)
+    assert np.all(np.abs(o.cpu().numpy() - ref) <= 2.0 ** -20 * np.abs(ref))
+
+
+def test_constant_v_and_zero_scale(ta):
+    q, k, _ = gen.random_problem(1, 2, 2, 200, 333, 128, seed=5)
+    c = 0.75
+    v = gen.bf16_from_f32(np.full(k.shape, c, dtype=np.float32))
+    for causal in (False, True):
+        o, _ = run(ta, q, k, v, causal, 0.088388)
+        assert float((o - c).abs().max()) <= 2 ** -8 * c
+    # scale 0: uniform weights over the visible keys, LSE = ln n_i
+    _, _, v = gen.random_problem(1, 2, 2, 200, 333, 128, seed=6)
+    o, lse = run(ta, q, k, v, True, 0.0)
+    n = np.minimum(333, np.arange(200) + 1 + 333 - 200)
+    assert np.abs(lse.cpu().numpy() - np.log(n)[None, None]).max() <= 1e-5
+    ro, _ = oracle.attn_fwd(q, k, v, True, 0.0)
+    assert np.abs(o.cpu().numpy() - ro).max() <= O_TOL
+
+
+def test_gqa_equals_repeated_heads_bitwise(ta):
+    q, k, v = gen.random_problem(1, 8, 2, 257, 257, 128, seed=7)
+    for causal in (False, True):
+        o1, l1 = run(ta, q, k, v, causal, 0.088388)
+        o2, l2 = run(ta, q, np.repeat(k, 4, axis=1), np.repeat(v, 4, axis=1), causal, 0.088388)
+        assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_permutation_invariance(ta):
+    q, k, v = gen.random_problem(1, 2, 2, 64, 500, 64, seed=8)
+    perm = np.random.default_rng(2).permutation(500)
+    o1, l1 = run(ta, q, k, v, False, 0.125)
+    o2, l2 = run(ta, q, k[:, :, perm], v[:, :, perm], False, 0.125)
+    assert float((o1 - o2).abs().max()) <= O_TOL and float((l1 - l2).abs().max()) <= LSE_TOL
+
+
+def test_deterministic_and_side_stream(ta):
+    q, k, v = gen.random_problem(2, 4, 4, 700, 700, 128, seed=9)
+    o1, l1 = run(ta, q, k, v, True, 0.088388)
+    o2, l2 = run(ta, q, k, v, True, 0.088388)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        o3, l3 = run(ta, q, k, v, True, 0.088388, stream=s)
+    s.synchronize()
+    assert torch.equal(o1, o3) and torch.equal(l1, l3)
+
+
+def test_binding_rejects_bad_arguments(ta):
+    q, k, v = (dev(a) for a in gen.random_problem(1, 2, 2, 64, 64, 64, seed=10))
+    with pytest.raises(ta.TileAttnError) as e:
+        ta.attn_fwd(q, k, v, scale=-1.0)
+    assert e.value.status == 5
+    o = torch.empty(1, 2, 64, 64, dtype=torch.float32, device="cuda")
+    lse = torch.empty(1, 2, 64, dtype=torch.float32, device="cuda")
+    # O aliasing Q's storage is refused before anything is launched
+    rc = ta.attn_fwd_raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), q.data_ptr(), lse.data_ptr(),
+                         1, 2, 2, 64, 64, 64, 0, 0.125, None)
+    assert rc == 6
+    rc = ta.attn_fwd_raw(q.data_ptr() + 2, k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                         lse.data_ptr(), 1, 2, 2, 64, 64, 64, 0, 0.125, None)
+    assert rc == 4
+    q96 = torch.zeros(1, 2, 64, 96, dtype=torch.bfloat16, device="cuda")
+    k96 = torch.zeros(1, 2, 64, 96, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ta.TileAttnError) as e:
+        ta.attn_fwd(q96, k96, k96)
+    assert e.value.status == 3
+    with pytest.raises(TypeError):
+        ta.attn_fwd(q.float(), k, v)
