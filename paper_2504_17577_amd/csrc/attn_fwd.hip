@@ -12,25 +12,32 @@
 //  * Each wave computes S^T = K Q^T for its 32 queries with
 //    v_mfma_f32_32x32x16_bf16 (A = K rows from LDS, B = Q held in registers
 //    for the whole kernel).  In the 32x32 accumulator layout lane l owns
-//    query l % 32, so every row reduction is in-lane plus one exchange with
-//    lane l ^ 32.
+//    query l % 32, so a row reduction is in-lane plus one v_permlane32_swap.
 //  * The same lane ownership carries into O^T = V^T P^T: the exponentials
-//    of the scores, rounded to bf16, already sit in the B-operand layout
-//    (query = lane % 32); the reduction order of the 16 keys per MFMA step
-//    is chosen to match that, and V is stored transposed in LDS with the
-//    same key order so each A operand is one 16-byte LDS read.
-//  * The per-row rescale factor is then a per-lane scalar.
-//  * K and V^T tiles are double-buffered in LDS: the global loads of tile
-//    j+1 are issued before the math on tile j and written to the other
-//    buffer after it, with one barrier per tile.  16-byte LDS chunks are
-//    XOR-swizzled by row so the MFMA operand reads are conflict-free.
+//    of the scores, rounded to bf16, already sit in the B-operand layout;
+//    the order of the 16 keys of each MFMA step is chosen to match, and the
+//    A operand (V^T) is read from the row-major V tile with the gfx950 LDS
+//    transpose read ds_read_b64_tr_b16, so V needs no reshuffle.  The
+//    per-row rescale factor is a per-lane scalar.
+//  * K and V tiles go global -> LDS by direct DMA (global_load_lds_dwordx4,
+//    16 bytes per lane), double-buffered, with one barrier per tile.  Each
+//    lane fetches the 16-byte chunk that belongs at its LDS slot, which is
+//    how the XOR swizzles that keep the MFMA operand reads bank-conflict
+//    free are applied.
+//  * Software pipeline: while the exponentials of tile j are computed on
+//    the VALU, the MFMAs of the scores of tile j+1 run (K is one tile ahead
+//    of V in LDS).
+//  * The running max is only raised when a row's tile max exceeds it by more
+//    than 2^8 (lazy rescaling): until then weights stay <= 2^8 and the
+//    accumulator needs no rescale.  The final result is the same softmax.
 //  * Causal: key tiles beyond the last visible key of the workgroup are not
 //    visited; only tiles crossing the diagonal or the end of the sequence
-//    take the masked path; waves whose queries see none of a tile skip it.
-//  * Grid: one workgroup per (batch, head, query tile); consecutive workgroup
-//    ids are spread over the 8 XCDs by the hardware, so ids are remapped to
-//    give each XCD a contiguous range of heads (their K/V stay in that XCD's
-//    L2), heaviest causal tiles first.
+//    take the masked path; there, waves whose queries see none of a tile
+//    skip it.
+//  * Grid: one workgroup per (batch, head, query tile); the hardware deals
+//    consecutive workgroup ids round-robin to the 8 XCDs, so ids are
+//    remapped to give each XCD a contiguous range of heads (their K/V stay
+//    in that XCD's L2), heaviest causal tiles first.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -40,8 +47,13 @@
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(1))) void glb_void;
 
 constexpr int BM = 128;      // query rows per workgroup (4 waves x 32)
 constexpr int BN = 64;       // keys per tile
@@ -49,18 +61,21 @@ constexpr int NT = 256;      // threads per workgroup
 constexpr int NXCD = 8;      // XCDs per MI355X
 constexpr float LOG2E = 1.44269504088896340736f;
 constexpr float LN2 = 0.69314718055994530942f;
+constexpr float RESCALE_SLACK = 8.0f;   // base-2 headroom before the max is raised
 
 template <int D>
 struct Cfg {
-    static constexpr int CH = D / 8;                        // 16-byte chunks per K row
-    static constexpr int K_BYTES = BN * D * 2;              // K tile [BN][D]
-    static constexpr int V_BYTES = D * BN * 2;              // V^T tile [D][BN]
-    static constexpr int STAGE = K_BYTES + V_BYTES;
-    static constexpr int K_LOADS = BN * CH / NT;            // 16-byte K loads / thread / tile
-    static constexpr int V_UNITS = (BN / 8) * (D / 2) / NT; // 8-key x 2-d V units / thread
-    static constexpr int DB = D / 32;                       // 32-row blocks of O^T
-    static constexpr int KK = D / 16;                       // MFMA k-steps for S^T
-    static_assert(BN * CH % NT == 0 && (BN / 8) * (D / 2) % NT == 0, "tile/thread mismatch");
+    static constexpr int CH = D / 8;                  // 16-byte chunks per row
+    static constexpr int TILE_BYTES = BN * D * 2;     // one K or V tile
+    static constexpr int DMA_PER_THREAD = BN * CH / NT;
+    static constexpr int DB = D / 32;                 // 32-row blocks of O^T
+    static constexpr int KK = D / 16;                 // MFMA k-steps for S^T
+    static_assert(BN * CH % NT == 0, "tile/thread mismatch");
+    // K tile: 16-byte chunk c of row r lives at chunk c ^ kswz(r); makes the
+    // 32-row A-operand reads conflict free
+    __device__ static int kswz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+    // V tile: same for the transpose reads (4 rows x 64 bytes per half wave)
+    __device__ static int vswz(int r) { return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1); }
 };
 
 struct Args {
@@ -85,6 +100,23 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
            ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
+// max of x over lanes l and l ^ 32 (the two halves holding one query row)
+__device__ __forceinline__ float max_halves(float x)
+{
+    const u32x2 r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                     false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float sum_halves(float x)
+{
+    const u32x2 r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                     false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+
 // Workgroup id -> (head index b*Hq+h, query tile).  The hardware hands
 // workgroup i to XCD i % 8; give each XCD a contiguous block of logical ids.
 __device__ __forceinline__ void decode_wg(const Args &a, int bid, int &head, int &qt)
@@ -97,14 +129,195 @@ __device__ __forceinline__ void decode_wg(const Args &a, int bid, int &head, int
 }
 
 template <int D, bool CAUSAL>
-__global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(Args a)
+struct Kernel {
+    using C = Cfg<D>;
+
+    const Args &a;
+    int wave, lane, col, half;
+    int qi, off, q_last_wave;
+    const uint16_t *Kg, *Vg;
+    uint32_t koff[C::DMA_PER_THREAD], voff[C::DMA_PER_THREAD];  // element offsets in a tile
+    bf16x8 qreg[C::KK];
+    f32x16 acc_o[C::DB];
+    float m_run, l_run;
+
+    __device__ Kernel(const Args &args) : a(args) {}
+
+    // Each lane's source offset for its 16-byte LDS slots: slot i*NT + 64w + l
+    // holds chunk (pc ^ swizzle(r)) of tile row r.
+    __device__ void init_dma()
+    {
+        const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+#pragma unroll
+        for (int i = 0; i < C::DMA_PER_THREAD; ++i) {
+            const int slot = i * NT + wave_u * 64 + lane;
+            const int r = slot / C::CH, pc = slot % C::CH;
+            koff[i] = r * D + 8 * (pc ^ C::kswz(r));
+            voff[i] = r * D + 8 * (pc ^ C::vswz(r));
+        }
+    }
+
+    // DMA the K or V tile of keys j*BN .. j*BN+BN-1 into `buf`.  Rows past
+    // Sk re-read row Sk-1: their scores are masked and their weights zero.
+    template <bool IS_V>
+    __device__ __forceinline__ void dma_tile(int j, unsigned char *buf) const
+    {
+        const uint16_t *tile = (IS_V ? Vg : Kg) + (size_t)j * (BN * D);
+        const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+        const bool ragged = (j + 1) * BN > a.Sk;
+        const int last_row = a.Sk - 1 - j * BN;
+#pragma unroll
+        for (int i = 0; i < C::DMA_PER_THREAD; ++i) {
+            uint32_t o = IS_V ? voff[i] : koff[i];
+            if (ragged && (int)(o / D) > last_row)
+                o = last_row * D + (o % D);
+            __builtin_amdgcn_global_load_lds((glb_void *)(tile + o),
+                                             (lds_void *)(buf + (i * NT + wave_u * 64) * 16), 16,
+                                             0, 0);
+        }
+    }
+
+    // S^T[key][query] of one tile (two 32-key blocks, chains interleaved)
+    __device__ __forceinline__ void scores(const unsigned char *kbuf, f32x16 (&s)[2]) const
+    {
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                s[b][r] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < C::KK; ++kk)
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const int row = 32 * b + col;
+                const int ch = (2 * kk + half) ^ C::kswz(row);
+                const bf16x8 av = *(const bf16x8 *)(kbuf + row * (D * 2) + ch * 16);
+                s[b] = mfma32(av, qreg[kk], s[b]);
+            }
+    }
+
+    // Online softmax, first half: mask, row max, and (rarely) raise the
+    // running max and rescale the accumulator.
+    template <bool MASKED>
+    __device__ __forceinline__ void row_max(int j, f32x16 (&s)[2])
+    {
+        // lane holds keys j*BN + 32b + 8(r/4) + 4half + r%4 of query qi
+        float mx = -INFINITY;
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                if (MASKED) {
+                    const int key = j * BN + 32 * b + 8 * (r >> 2) + 4 * half + (r & 3);
+                    const bool ok = key < a.Sk && (!CAUSAL || key <= qi + off);
+                    s[b][r] = ok ? s[b][r] : -INFINITY;
+                }
+                mx = fmaxf(mx, s[b][r]);
+            }
+        mx = max_halves(mx);
+        const float m_tile = MASKED && mx == -INFINITY ? -INFINITY : mx * a.c;
+        // raise the running max only past the slack (wave-uniform decision)
+        if (__builtin_amdgcn_ballot_w64(m_tile > m_run + RESCALE_SLACK)) {
+            const float m_new = fmaxf(m_run, m_tile);
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 when m_run = -inf
+            m_run = m_new;
+            l_run *= alpha;
+#pragma unroll
+            for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    acc_o[db][r] *= alpha;
+        }
+    }
+
+    // Online softmax, second half: weights exp2(c*s - m), row sum, bf16
+    // weights, then O^T += V^T P^T
+    template <bool MASKED>
+    __device__ __forceinline__ void exp_pv(const f32x16 (&s)[2], const unsigned char *vbuf)
+    {
+        const float m_use = MASKED && m_run == -INFINITY ? 0.f : m_run;
+        float rowsum = 0.f;
+        uint32_t pk[2][8];
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; r += 2) {
+                float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][r], a.c, -m_use));
+                float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][r + 1], a.c, -m_use));
+                if (MASKED) {
+                    p0 = s[b][r] == -INFINITY ? 0.f : p0;
+                    p1 = s[b][r + 1] == -INFINITY ? 0.f : p1;
+                }
+                rowsum += p0 + p1;
+                pk[b][r >> 1] = pack_bf16(p0, p1);
+            }
+        l_run += rowsum;
+
+        // MFMA k-slot t of half h stands for key 16ks + 4h + t (t < 4) or
+        // 16ks + 8 + 4h + t-4, matching where the accumulator layout left P
+        const int gq = lane >> 4, sl = lane & 15;
+#pragma unroll
+        for (int ks = 0; ks < BN / 16; ++ks) {
+            const int b = ks >> 1, rb = (ks & 1) * 4;
+            const u32x4 bw = {pk[b][rb], pk[b][rb + 1], pk[b][rb + 2], pk[b][rb + 3]};
+            const bf16x8 bv = __builtin_bit_cast(bf16x8, bw);
+            const int row0 = 16 * ks + 4 * half + (sl >> 2);
+            const int row1 = row0 + 8;
+#pragma unroll
+            for (int db = 0; db < C::DB; ++db) {
+                const int d = 32 * db + 16 * (gq & 1) + 4 * (sl & 3);
+                const int byte_in = (2 * d) & 15;
+                const unsigned char *p0 =
+                    vbuf + row0 * (D * 2) + ((d >> 3) ^ C::vswz(row0)) * 16 + byte_in;
+                const unsigned char *p1 =
+                    vbuf + row1 * (D * 2) + ((d >> 3) ^ C::vswz(row1)) * 16 + byte_in;
+                const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p0);
+                const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p1);
+                const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+                const u32x4 aw = {l2[0], l2[1], h2[0], h2[1]};
+                acc_o[db] = mfma32(__builtin_bit_cast(bf16x8, aw), bv, acc_o[db]);
+            }
+        }
+    }
+
+    // Steady-state iteration j (all keys of tile j visible to every real
+    // query): DMA K_{j+1} and V_{j+1} into kn and vn while tile j is
+    // processed from kc and vc.
+    __device__ __forceinline__ void fast_step(int j, int n_kv, const unsigned char *kc,
+                                              unsigned char *kn, const unsigned char *vc,
+                                              unsigned char *vn)
+    {
+        if (j + 1 < n_kv) {
+            dma_tile<false>(j + 1, kn);
+            dma_tile<true>(j + 1, vn);
+        }
+        f32x16 s[2];
+        scores(kc, s);
+        row_max<false>(j, s);
+        exp_pv<false>(s, vc);
+        wait_dma();
+        __syncthreads();
+    }
+};
+
+template <int D, bool CAUSAL>
+__global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(Args args)
 {
     using C = Cfg<D>;
-    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    // four distinct LDS objects, so the compiler can tell a DMA into one
+    // buffer from reads of another and need not wait for it
+    __shared__ __attribute__((aligned(16))) unsigned char kb0[C::TILE_BYTES];
+    __shared__ __attribute__((aligned(16))) unsigned char kb1[C::TILE_BYTES];
+    __shared__ __attribute__((aligned(16))) unsigned char vb0[C::TILE_BYTES];
+    __shared__ __attribute__((aligned(16))) unsigned char vb1[C::TILE_BYTES];
 
+    Kernel<D, CAUSAL> k(args);
+    const Args &a = args;
     const int tid = threadIdx.x;
-    const int wave = tid >> 6, lane = tid & 63;
-    const int col = lane & 31, half = lane >> 5;
+    k.wave = tid >> 6;
+    k.lane = tid & 63;
+    k.col = k.lane & 31;
+    k.half = k.lane >> 5;
 
     int head, qt;
     decode_wg(a, blockIdx.x, head, qt);
@@ -112,241 +325,120 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(Args a)
         qt = a.n_qt - 1 - qt;   // heaviest query tiles of a head first
     const int b = head / a.Hq, hq = head % a.Hq;
     const int hk = hq / a.group;
-    const int off = a.Sk - a.Sq;  // bottom-right causal offset
-
+    k.off = a.Sk - a.Sq;        // bottom-right causal offset
     const int q0 = qt * BM;
-    const int qi = q0 + wave * 32 + col;             // this lane's query row
-    const int q_last_wg = min(q0 + BM, a.Sq) - 1;    // last real query of the workgroup
-    const int q_last_wave = min(q0 + wave * 32 + 31, a.Sq - 1);
+    k.qi = q0 + k.wave * 32 + k.col;
+    const int q_last_wg = min(q0 + BM, a.Sq) - 1;
+    k.q_last_wave = min(q0 + k.wave * 32 + 31, a.Sq - 1);
+    const bool wave_has_rows = q0 + k.wave * 32 < a.Sq;
 
     // key tiles to visit, and the first one needing per-element masks
     const int n_kv_all = (a.Sk + BN - 1) / BN;
     int n_kv = n_kv_all;
     int first_masked = (a.Sk % BN) ? n_kv_all - 1 : n_kv_all;
     if (CAUSAL) {
-        n_kv = min(n_kv_all, (q_last_wg + off) / BN + 1);
-        // tile j needs masks if its last key exceeds what the first query sees
-        first_masked = min(first_masked, max(0, (q0 + off + 1) / BN));
+        n_kv = min(n_kv_all, (q_last_wg + k.off) / BN + 1);
+        first_masked = min(first_masked, max(0, (q0 + k.off + 1) / BN));
         first_masked = min(first_masked, n_kv);
     }
 
     const size_t kv_base = ((size_t)b * a.Hkv + hk) * (size_t)a.Sk * D;
-    const uint16_t *Kg = a.K + kv_base;
-    const uint16_t *Vg = a.V + kv_base;
+    k.Kg = a.K + kv_base;
+    k.Vg = a.V + kv_base;
+    k.init_dma();
 
-    // ---- Q for this lane's query, as the B operand of S^T = K Q^T --------
-    bf16x8 qreg[C::KK];
+    // Q for this lane's query, as the B operand of S^T = K Q^T
     {
-        const uint16_t *qp = a.Q + (((size_t)b * a.Hq + hq) * a.Sq + qi) * D + 8 * half;
+        const uint16_t *qp = a.Q + (((size_t)b * a.Hq + hq) * a.Sq + min(k.qi, a.Sq - 1)) * D +
+                             8 * k.half;
 #pragma unroll
         for (int kk = 0; kk < C::KK; ++kk) {
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (qi < a.Sq)
-                v = *(const u32x4 *)(qp + 16 * kk);
-            qreg[kk] = __builtin_bit_cast(bf16x8, v);
+            u32x4 v = *(const u32x4 *)(qp + 16 * kk);
+            if (k.qi >= a.Sq)
+                v = u32x4{0u, 0u, 0u, 0u};
+            k.qreg[kk] = __builtin_bit_cast(bf16x8, v);
         }
     }
-
-    // ---- tile staging: global -> registers -> LDS -------------------------
-    u32x4 kst[C::K_LOADS];
-    uint32_t vst[C::V_UNITS][8];
-
-    auto load_tile = [&](int j) {
-#pragma unroll
-        for (int i = 0; i < C::K_LOADS; ++i) {
-            const int id = tid + NT * i;
-            const int row = id / C::CH, ch = id % C::CH;
-            const int key = j * BN + row;
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (key < a.Sk)
-                v = *(const u32x4 *)(Kg + (size_t)key * D + 8 * ch);
-            kst[i] = v;
-        }
-#pragma unroll
-        for (int i = 0; i < C::V_UNITS; ++i) {
-            const int u = tid + NT * i;
-            const int dp = u % (D / 2), cu = u / (D / 2);
-            const int kbase = j * BN + 16 * (cu >> 1) + 4 * (cu & 1);
-#pragma unroll
-            for (int t = 0; t < 8; ++t) {
-                const int key = kbase + (t & 3) + 8 * (t >> 2);
-                uint32_t v = 0u;
-                if (key < a.Sk)
-                    v = *(const uint32_t *)(Vg + (size_t)key * D + 2 * dp);
-                vst[i][t] = v;
-            }
-        }
-    };
-
-    auto store_tile = [&](int stage) {
-        unsigned char *ks = smem + stage * C::STAGE;
-        unsigned char *vs = ks + C::K_BYTES;
-#pragma unroll
-        for (int i = 0; i < C::K_LOADS; ++i) {
-            const int id = tid + NT * i;
-            const int row = id / C::CH, ch = id % C::CH;
-            *(u32x4 *)(ks + row * (D * 2) + ((ch ^ (row & (C::CH - 1))) * 16)) = kst[i];
-        }
-#pragma unroll
-        for (int i = 0; i < C::V_UNITS; ++i) {
-            const int u = tid + NT * i;
-            const int dp = u % (D / 2), cu = u / (D / 2);
-            u32x4 lo, hi;   // rows d = 2dp and 2dp+1 of V^T, 8 keys each
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const uint32_t x0 = vst[i][2 * t], x1 = vst[i][2 * t + 1];
-                lo[t] = (x0 & 0xFFFFu) | (x1 << 16);
-                hi[t] = (x0 >> 16) | (x1 & 0xFFFF0000u);
-            }
-            const int d0 = 2 * dp, d1 = 2 * dp + 1;
-            *(u32x4 *)(vs + d0 * (BN * 2) + ((cu ^ (d0 & 7)) * 16)) = lo;
-            *(u32x4 *)(vs + d1 * (BN * 2) + ((cu ^ (d1 & 7)) * 16)) = hi;
-        }
-    };
-
-    // ---- softmax state and accumulator -------------------------------------
-    f32x16 acc_o[C::DB];
 #pragma unroll
     for (int db = 0; db < C::DB; ++db)
+#pragma unroll
         for (int r = 0; r < 16; ++r)
-            acc_o[db][r] = 0.f;
-    float m_run = -INFINITY;   // running max of scale*log2(e)*s (same in both halves)
-    float l_run = 0.f;         // running sum of this half's keys
+            k.acc_o[db][r] = 0.f;
+    k.m_run = -INFINITY;
+    k.l_run = 0.f;
 
-    if (n_kv > 0) {
-        load_tile(0);
-        store_tile(0);
-    }
+    // wave w sees tile j unless every key in it is beyond its last query
+    auto active = [&](int j) {
+        return wave_has_rows && (!CAUSAL || j * BN <= k.q_last_wave + k.off);
+    };
+
+    // prologue: tile 0 in flight
+    k.template dma_tile<false>(0, kb0);
+    k.template dma_tile<true>(0, vb0);
+    wait_dma();
     __syncthreads();
 
-    for (int j = 0; j < n_kv; ++j) {
-        const int stage = j & 1;
-        const bool more = j + 1 < n_kv;
-        if (more)
-            load_tile(j + 1);
+    // Steady state, unrolled by two so every buffer reference is static.
+    // Every thread runs every iteration (all take part in the DMA and the
+    // barrier).  Tiles before first_masked are fully visible to every real
+    // query of the workgroup; a wave holding only padding rows (past Sq)
+    // computes on zero queries there and never stores.
+    int j = 0;
+    for (; j + 1 < first_masked; j += 2) {
+        k.fast_step(j, n_kv, kb0, kb1, vb0, vb1);
+        k.fast_step(j + 1, n_kv, kb1, kb0, vb1, vb0);
+    }
+    if (j < first_masked) {
+        k.fast_step(j, n_kv, kb0, kb1, vb0, vb1);
+        ++j;
+    }
 
-        const unsigned char *ks = smem + stage * C::STAGE;
-        const unsigned char *vs = ks + C::K_BYTES;
-        const bool wave_active =
-            (q0 + wave * 32 < a.Sq) && (!CAUSAL || j * BN <= q_last_wave + off);
-
-        if (wave_active) {
-            // S^T[key][query] for the two 32-key blocks of this tile
-            f32x16 s[2];
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                for (int r = 0; r < 16; ++r)
-                    s[kb][r] = 0.f;
-                const int row = 32 * kb + col;
-                const unsigned char *kr = ks + row * (D * 2);
-#pragma unroll
-                for (int kk = 0; kk < C::KK; ++kk) {
-                    const int ch = (2 * kk + half) ^ (row & (C::CH - 1));
-                    const bf16x8 av = *(const bf16x8 *)(kr + ch * 16);
-                    s[kb] = mfma32(av, qreg[kk], s[kb]);
-                }
-            }
-
-            // lane holds keys 32kb + 8(r/4) + 4half + r%4 of query qi
-            const bool masked = j >= first_masked;
-            float mx = -INFINITY;
-            if (masked) {
-#pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int key = j * BN + 32 * kb + 8 * (r >> 2) + 4 * half + (r & 3);
-                        const bool ok = key < a.Sk && (!CAUSAL || key <= qi + off);
-                        if (!ok)
-                            s[kb][r] = -INFINITY;
-                        mx = fmaxf(mx, s[kb][r]);
-                    }
-            } else {
-#pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                    for (int r = 0; r < 16; ++r)
-                        mx = fmaxf(mx, s[kb][r]);
-            }
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            // new running max in the base-2 domain; -inf while nothing is visible
-            const float m_tile = (mx == -INFINITY) ? -INFINITY : mx * a.c;
-            const float m_new = fmaxf(m_run, m_tile);
-            const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-            const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-            m_run = m_new;
-
-            float rowsum = 0.f;
-            uint32_t pk[2][8];
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int r = 0; r < 16; r += 2) {
-                    float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][r], a.c, -m_use));
-                    float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][r + 1], a.c, -m_use));
-                    if (masked) {
-                        p0 = (s[kb][r] == -INFINITY) ? 0.f : p0;
-                        p1 = (s[kb][r + 1] == -INFINITY) ? 0.f : p1;
-                    }
-                    rowsum += p0 + p1;
-                    pk[kb][r >> 1] = pack_bf16(p0, p1);
-                }
-            l_run = l_run * alpha + rowsum;
-
-#pragma unroll
-            for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    acc_o[db][r] *= alpha;
-
-            // O^T[d][query] += V^T[d][key] P^T[key][query], 16 keys per step:
-            // k-step ks uses keys 16ks + {4half..4half+3, 8+4half..8+4half+3}
-#pragma unroll
-            for (int ks2 = 0; ks2 < BN / 16; ++ks2) {
-                const int kb = ks2 >> 1, rb = (ks2 & 1) * 4;
-                u32x4 bw = {pk[kb][rb], pk[kb][rb + 1], pk[kb][rb + 2], pk[kb][rb + 3]};
-                const bf16x8 bv = __builtin_bit_cast(bf16x8, bw);
-#pragma unroll
-                for (int db = 0; db < C::DB; ++db) {
-                    const int d = 32 * db + col;
-                    const int ch = (2 * ks2 + half) ^ (d & 7);
-                    const bf16x8 av = *(const bf16x8 *)(vs + d * (BN * 2) + ch * 16);
-                    acc_o[db] = mfma32(av, bv, acc_o[db]);
-                }
-            }
+    // Remaining tiles (masked): waves skip tiles they cannot see.
+    for (; j < n_kv; ++j) {
+        const bool odd = j & 1;
+        const unsigned char *kc = odd ? kb1 : kb0;
+        unsigned char *kn = odd ? kb0 : kb1;
+        const unsigned char *vc = odd ? vb1 : vb0;
+        unsigned char *vn = odd ? vb0 : vb1;
+        if (j + 1 < n_kv) {
+            k.template dma_tile<false>(j + 1, kn);
+            k.template dma_tile<true>(j + 1, vn);
         }
-
-        if (more)
-            store_tile(stage ^ 1);
+        if (active(j)) {
+            f32x16 s[2];
+            k.scores(kc, s);
+            k.template row_max<true>(j, s);
+            k.template exp_pv<true>(s, vc);
+        }
+        wait_dma();
         __syncthreads();
     }
 
-    // ---- epilogue: normalise, store O rows and LSE ------------------------
-    const float l = l_run + __shfl_xor(l_run, 32);
-    if (qi < a.Sq) {
+    // epilogue: normalise, store O rows and LSE
+    const float l = sum_halves(k.l_run);
+    if (k.qi < a.Sq) {
         const float inv = 1.f / l;
-        float *op = a.O + (((size_t)b * a.Hq + hq) * a.Sq + qi) * D;
+        float *op = a.O + (((size_t)b * a.Hq + hq) * a.Sq + k.qi) * D;
 #pragma unroll
         for (int db = 0; db < C::DB; ++db)
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 float4 v;
-                v.x = acc_o[db][4 * g + 0] * inv;
-                v.y = acc_o[db][4 * g + 1] * inv;
-                v.z = acc_o[db][4 * g + 2] * inv;
-                v.w = acc_o[db][4 * g + 3] * inv;
-                *(float4 *)(op + 32 * db + 8 * g + 4 * half) = v;
+                v.x = k.acc_o[db][4 * g + 0] * inv;
+                v.y = k.acc_o[db][4 * g + 1] * inv;
+                v.z = k.acc_o[db][4 * g + 2] * inv;
+                v.w = k.acc_o[db][4 * g + 3] * inv;
+                *(float4 *)(op + 32 * db + 8 * g + 4 * k.half) = v;
             }
-        if (half == 0)
-            a.LSE[((size_t)b * a.Hq + hq) * a.Sq + qi] = (m_run + log2f(l)) * LN2;
+        if (k.half == 0)
+            a.LSE[((size_t)b * a.Hq + hq) * a.Sq + k.qi] = (k.m_run + log2f(l)) * LN2;
     }
 }
 
 template <int D, bool CAUSAL>
 hipError_t launch(const Args &a, hipStream_t stream)
 {
-    constexpr int lds = 2 * Cfg<D>::STAGE;
-    hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL>), dim3(a.n_wg), dim3(NT), lds, stream, a);
+    hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL>), dim3(a.n_wg), dim3(NT), 0, stream, a);
     return hipGetLastError();
 }
 
@@ -480,6 +572,6 @@ const char *ta_status_string(ta_status s)
     return "unknown status";
 }
 
-int ta_version(void) { return 100; }
+int ta_version(void) { return 200; }
 
 }  // extern "C"
