@@ -51,6 +51,8 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(1))) void glb_void;
@@ -62,6 +64,9 @@ constexpr int NXCD = 8;      // XCDs per MI355X
 constexpr float LOG2E = 1.44269504088896340736f;
 constexpr float LN2 = 0.69314718055994530942f;
 constexpr float RESCALE_SLACK = 8.0f;   // base-2 headroom before the max is raised
+// word 3 of a raw (unswizzled, stride 0) buffer resource on CDNA: 32-bit
+// data format, loads past num_records return zero
+[[maybe_unused]] constexpr int BUF_RSRC_WORD3 = 0x00020000;
 
 template <int D>
 struct Cfg {
@@ -95,9 +100,8 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c)
 
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
 {
-    __bf16 a = (__bf16)lo, b = (__bf16)hi;   // round to nearest even
-    return (uint32_t)__builtin_bit_cast(uint16_t, a) |
-           ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+    // one v_cvt_pk_bf16_f32: both halves rounded to nearest even
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 // max of x over lanes l and l ^ 32 (the two halves holding one query row)
@@ -136,15 +140,15 @@ struct Kernel {
     int wave, lane, col, half;
     int qi, off, q_last_wave;
     const uint16_t *Kg, *Vg;
-    uint32_t koff[C::DMA_PER_THREAD], voff[C::DMA_PER_THREAD];  // element offsets in a tile
+    uint32_t koff[C::DMA_PER_THREAD], voff[C::DMA_PER_THREAD];  // byte offsets in a tile
     bf16x8 qreg[C::KK];
     f32x16 acc_o[C::DB];
     float m_run, l_run;
 
     __device__ Kernel(const Args &args) : a(args) {}
 
-    // Each lane's source offset for its 16-byte LDS slots: slot i*NT + 64w + l
-    // holds chunk (pc ^ swizzle(r)) of tile row r.
+    // Each lane's source byte offset (within a tile) for its 16-byte LDS
+    // slots: slot i*NT + 64w + l holds chunk (pc ^ swizzle(r)) of tile row r.
     __device__ void init_dma()
     {
         const int wave_u = __builtin_amdgcn_readfirstlane(wave);
@@ -152,29 +156,44 @@ struct Kernel {
         for (int i = 0; i < C::DMA_PER_THREAD; ++i) {
             const int slot = i * NT + wave_u * 64 + lane;
             const int r = slot / C::CH, pc = slot % C::CH;
-            koff[i] = r * D + 8 * (pc ^ C::kswz(r));
-            voff[i] = r * D + 8 * (pc ^ C::vswz(r));
+            koff[i] = 2 * (r * D + 8 * (pc ^ C::kswz(r)));
+            voff[i] = 2 * (r * D + 8 * (pc ^ C::vswz(r)));
         }
     }
 
-    // DMA the K or V tile of keys j*BN .. j*BN+BN-1 into `buf`.  Rows past
-    // Sk re-read row Sk-1: their scores are masked and their weights zero.
+    // DMA the K or V tile of keys j*BN .. j*BN+BN-1 into `buf` with
+    // buffer_load_dwordx4 ... lds.  The buffer resource starts at the tile
+    // and ends at the end of this (batch, head) slice; on the ragged last
+    // tile rows past Sk re-read row Sk-1 (their scores are masked and their
+    // weights zero), so no lane addresses past the slice.
     template <bool IS_V>
     __device__ __forceinline__ void dma_tile(int j, unsigned char *buf) const
     {
+#if __HIP_DEVICE_COMPILE__   // buffer-resource builtins exist in the device pass only
+        const uint32_t tile_bytes = BN * D * 2;
         const uint16_t *tile = (IS_V ? Vg : Kg) + (size_t)j * (BN * D);
+        const uint32_t left = (uint32_t)a.Sk * (D * 2) - (uint32_t)j * tile_bytes;
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc((void *)tile, 0, (int)left, BUF_RSRC_WORD3);
         const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-        const bool ragged = (j + 1) * BN > a.Sk;
-        const int last_row = a.Sk - 1 - j * BN;
+        if ((j + 1) * BN <= a.Sk) {
 #pragma unroll
-        for (int i = 0; i < C::DMA_PER_THREAD; ++i) {
-            uint32_t o = IS_V ? voff[i] : koff[i];
-            if (ragged && (int)(o / D) > last_row)
-                o = last_row * D + (o % D);
-            __builtin_amdgcn_global_load_lds((glb_void *)(tile + o),
-                                             (lds_void *)(buf + (i * NT + wave_u * 64) * 16), 16,
-                                             0, 0);
+            for (int i = 0; i < C::DMA_PER_THREAD; ++i)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rs, (lds_void *)(buf + (i * NT + wave_u * 64) * 16), 16,
+                    IS_V ? voff[i] : koff[i], 0, 0, 0);
+        } else {
+            const int last_row = a.Sk - 1 - j * BN;
+#pragma unroll
+            for (int i = 0; i < C::DMA_PER_THREAD; ++i) {
+                uint32_t o = IS_V ? voff[i] : koff[i];
+                if ((int)(o / (2 * D)) > last_row)
+                    o = last_row * (2 * D) + (o % (2 * D));
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rs, (lds_void *)(buf + (i * NT + wave_u * 64) * 16), 16, o, 0, 0, 0);
+            }
         }
+#endif
     }
 
     // S^T[key][query] of one tile (two 32-key blocks, chains interleaved)
