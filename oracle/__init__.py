@@ -46,7 +46,7 @@ def load(path: str | None = None):
 
 def default_threads() -> int:
     """Host threads for the oracle: the cores this process may run on,
-    capped at 16 (a GPU machine's CPU share)."""
+    capped at 16 threads."""
     try:
         n = len(os.sched_getaffinity(0))
     except AttributeError:
