@@ -70,9 +70,10 @@ class Workload:
         return s
 
 
-# The five workloads: a tiny correctness case, a causal D=64 case, the dense
-# D=128 throughput case, a long causal case with peaky keys and a grouped-query
-# causal case.  All draw Q/K/V i.i.d. N(0,1) in bf16 with scale 1/sqrt(D).
+# Workloads: a tiny correctness case, a causal D=64 case, the dense D=128
+# throughput case, a long causal case with peaky keys, a grouped-query causal
+# case, and the paper's five FlashAttention benchmark shapes.  All draw Q/K/V
+# i.i.d. N(0,1) in bf16 with scale 1/sqrt(D).
 WORKLOADS = {
     w.name: w
     for w in (
@@ -82,6 +83,13 @@ WORKLOADS = {
         Workload("causal_peaky_d128_s8k", 3, 1, 32, 32, 8192, 8192, 128, True,
                  peaky_every=64, peaky_factor=8.0),
         Workload("gqa4_causal_d128_s4k", 4, 2, 32, 8, 4096, 4096, 128, True),
+        # the paper's FlashAttention benchmark shapes (table "FlashAttention
+        # shapes in our benchmark"): batch 1, 32 heads, head dim 128
+        Workload("paper_fa0_s512_causal", 10, 1, 32, 32, 512, 512, 128, True),
+        Workload("paper_fa1_s512", 11, 1, 32, 32, 512, 512, 128, False),
+        Workload("paper_fa2_s1k_causal", 12, 1, 32, 32, 1024, 1024, 128, True),
+        Workload("paper_fa3_s1k", 13, 1, 32, 32, 1024, 1024, 128, False),
+        Workload("paper_fa4_s4k_causal", 14, 1, 32, 32, 4096, 4096, 128, True),
     )
 }
 
