@@ -9,6 +9,9 @@ bounded sample of the same workload as a reported baseline.
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
   python bench.py --copy-probe      # plain device copy of known size, for
                                     # scaling rocprofv3 FETCH_SIZE/WRITE_SIZE
+  python bench.py --sustain 8 [--gemm-reference]
+                                    # run the step back to back for 8 s while
+                                    # sampling board power and XCD clocks
 """
 from __future__ import annotations
 
@@ -91,6 +94,73 @@ def cpu_baseline(w, q, k, v, budget_s: float = 15.0):
     }
 
 
+class PowerSampler:
+    """Samples socket power and the eight XCD shader clocks with ``amd-smi
+    metric -p -c`` in a background thread (a child process per sample)."""
+
+    def __init__(self):
+        import threading
+        self.samples = []
+        self._stop = threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True)
+
+    def _run(self):
+        import subprocess
+        while not self._stop.is_set():
+            try:
+                out = subprocess.run(["amd-smi", "metric", "-p", "-c"], capture_output=True,
+                                     text=True, timeout=10).stdout
+            except (OSError, subprocess.SubprocessError):
+                return
+            p = re.search(r"SOCKET_POWER:\s*(\d+)", out)
+            clk = [int(c) for c in re.findall(r"GFX_\d+:\s*\n\s*CLK:\s*(\d+)", out)]
+            if p and clk:
+                self.samples.append((time.perf_counter(), int(p.group(1)), clk))
+            self._stop.wait(0.2)
+
+    def __enter__(self):
+        self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        self._thread.join()
+
+    def summary(self, t0: float, t1: float):
+        ss = [s for s in self.samples if t0 <= s[0] <= t1]
+        if not ss:
+            return None
+        n_x = min(len(s[2]) for s in ss)
+        clk = [sum(s[2][x] for s in ss) / len(ss) for x in range(n_x)]
+        return {"socket_power_w": round(sum(s[1] for s in ss) / len(ss), 1),
+                "xcd_clock_mhz_mean": round(sum(clk) / n_x, 1),
+                "xcd_clock_mhz_min": round(min(clk), 1), "xcd_clock_mhz_max": round(max(clk), 1),
+                "samples": len(ss)}
+
+
+def sustained(torch, fn, flops: float, seconds: float, sampler: PowerSampler):
+    """Run ``fn`` back to back for about ``seconds`` s; report the rate and the
+    power/clock samples taken after the first second (clocks settle)."""
+    fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    n = 0
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(20):
+            fn()
+        torch.cuda.synchronize()
+        n += 20
+    end.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = start.elapsed_time(end) / n
+    return {"tflops": round(flops / (ms * 1e-3) / 1e12, 2), "ms_per_call": round(ms, 5),
+            "calls": n, **(sampler.summary(t0 + 1.0, t1) or {})}
+
+
 def copy_probe(torch, mib: int = 1024, reps: int = 5):
     n = mib * (1 << 20) // 4
     src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -111,6 +181,12 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--sustain", type=float, default=0.0,
+                    help="also run the step back to back for this many seconds while "
+                         "sampling board power and XCD clocks (amd-smi)")
+    ap.add_argument("--gemm-reference", action="store_true",
+                    help="with --sustain: the same for a bf16 8192^3 torch.matmul, as a "
+                         "reference for what the matrix cores sustain at the power limit")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -196,6 +272,19 @@ def main():
         "wall_s_timed": round(wall, 4),
         "check": {"max_abs_dO": err_o, "max_abs_dLSE": err_l, "rows": len(rows)},
     }
+    if args.sustain > 0:
+        with PowerSampler() as sampler:
+            result["sustained"] = sustained(torch, step, w.flops(), args.sustain, sampler)
+            if args.gemm_reference:
+                time.sleep(2.0)
+                n = 8192
+                ga = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+                gb = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+                gc = torch.empty_like(ga)
+                result["sustained_gemm_reference"] = {
+                    "op": f"torch.matmul bf16 {n}x{n}x{n}",
+                    **sustained(torch, lambda: torch.matmul(ga, gb, out=gc), 2.0 * n ** 3,
+                                args.sustain, sampler)}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, q, k, v)
     print(json.dumps(result), flush=True)
