@@ -6,7 +6,8 @@ flops over visible query-key pairs), the roofline position of the kernel
 against the dense bf16 MFMA peak, and the fp64 CPU oracle's throughput on a
 bounded sample of the same workload as a reported baseline.
 
-  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--out f32|bf16]
+                  [--splits 1|N|auto] [--no-cpu-baseline]
   python bench.py --copy-probe      # plain device copy of known size, for
                                     # scaling rocprofv3 FETCH_SIZE/WRITE_SIZE
   python bench.py --sustain 8 [--gemm-reference]
@@ -179,6 +180,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(gen.WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--out", choices=("f32", "bf16"), default="f32",
+                    help="output dtype of O: attn_fwd (f32) or attn_fwd_bf16out (bf16)")
+    ap.add_argument("--splits", default="1",
+                    help="key splits per query tile: 1 (attn_fwd), N or auto "
+                         "(attn_fwd_split with ta_split_heuristic; workspace allocated "
+                         "before the timed region)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
     ap.add_argument("--sustain", type=float, default=0.0,
@@ -205,13 +212,28 @@ def main():
     w = gen.WORKLOADS[args.workload]
     q, k, v = gen.make_inputs(w, seed=args.seed)
     dq, dk, dv = to_device(q, torch), to_device(k, torch), to_device(v, torch)
-    o = torch.empty((w.B, w.Hq, w.Sq, w.D), dtype=torch.float32, device="cuda")
+    o_bf16 = args.out == "bf16"
+    o = torch.empty((w.B, w.Hq, w.Sq, w.D), dtype=torch.bfloat16 if o_bf16 else torch.float32,
+                    device="cuda")
     lse = torch.empty((w.B, w.Hq, w.Sq), dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
 
-    def step():
-        tileattn.attn_fwd(dq, dk, dv, causal=w.causal, scale=w.scale, out=o, lse=lse,
-                          stream=stream)
+    n_split = (tileattn.ta_split_heuristic(w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal)
+               if args.splits == "auto" else int(args.splits))
+    if n_split > 1:
+        ws = torch.empty(max(16, tileattn.ta_split_workspace_bytes(w.B, w.Hq, w.Sq, w.D, n_split)),
+                         dtype=torch.uint8, device="cuda")
+        o_dt = torch.bfloat16 if o_bf16 else torch.float32
+
+        def step():
+            tileattn.attn_fwd_split(dq, dk, dv, causal=w.causal, scale=w.scale,
+                                    num_splits=n_split, out=o, lse=lse, workspace=ws,
+                                    out_dtype=o_dt, stream=stream)
+    else:
+        fwd = tileattn.attn_fwd_bf16out if o_bf16 else tileattn.attn_fwd
+
+        def step():
+            fwd(dq, dk, dv, causal=w.causal, scale=w.scale, out=o, lse=lse, stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -222,7 +244,7 @@ def main():
     rows = [(0, 0, 0), (w.B - 1, w.Hq - 1, w.Sq - 1), (w.B // 2, w.Hq // 2, w.Sq // 2)]
     ro, rl = oracle.attn_rows(q, k, v, w.causal, w.scale, rows)
     idx = tuple(torch.tensor(c) for c in zip(*rows))
-    err_o = float(np.abs(o[idx].cpu().numpy() - ro).max())
+    err_o = float(np.abs(o[idx].float().cpu().numpy() - ro).max())
     err_l = float(np.abs(lse[idx].cpu().numpy() - rl).max())
     if not (err_o <= 2e-2 and err_l <= 1e-3):
         raise SystemExit(f"bench: result check failed (max|dO|={err_o}, max|dLSE|={err_l})")
@@ -241,7 +263,7 @@ def main():
     ms = start.elapsed_time(end) / args.steps
     tflops = w.flops() / (ms * 1e-3) / 1e12
 
-    traffic = read_traffic(w.name)
+    traffic = None if (o_bf16 or n_split > 1) else read_traffic(w.name)
     result = {
         "metric": METRIC,
         "value": round(tflops, 2),
@@ -254,6 +276,8 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
+        "out_dtype": args.out,
+        "splits": n_split,
         "data": "synthetic",
         "config": {"workload": w.name, "shape": w.describe(), "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv,
                    "Sq": w.Sq, "Sk": w.Sk, "D": w.D, "causal": w.causal, "seed": args.seed,
@@ -267,7 +291,7 @@ def main():
             "unit": "TFLOP/s",
             "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic,
-            "hbm_gbs_algorithmic": round(w.bytes() / (ms * 1e-3) / 1e9, 1),
+            "hbm_gbs_algorithmic": round(w.bytes(2 if o_bf16 else 4) / (ms * 1e-3) / 1e9, 1),
         },
         "wall_s_timed": round(wall, 4),
         "check": {"max_abs_dO": err_o, "max_abs_dLSE": err_l, "rows": len(rows)},

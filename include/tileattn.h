@@ -28,6 +28,7 @@
 #ifndef TILEATTN_H
 #define TILEATTN_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -43,7 +44,8 @@ typedef enum {
     TA_ERR_MISALIGNED = 4,    /* a pointer is not 16-byte aligned                           */
     TA_ERR_INVALID_SCALE = 5, /* scale is negative, NaN or infinite                         */
     TA_ERR_ALIASING = 6,      /* O or LSE overlaps an input or each other                   */
-    TA_ERR_LAUNCH = 7         /* the HIP runtime reported an error for the launch           */
+    TA_ERR_LAUNCH = 7,        /* the HIP runtime reported an error for the launch           */
+    TA_ERR_WORKSPACE = 8      /* attn_fwd_split: workspace NULL or smaller than required    */
 } ta_status;
 
 /*
@@ -69,6 +71,64 @@ typedef enum {
 ta_status attn_fwd(const void *Q, const void *K, const void *V, float *O, float *LSE,
                    int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, float scale,
                    void *stream);
+
+/*
+ * attn_fwd_bf16out — attn_fwd with O written in bf16 instead of fp32.
+ *
+ *   O    device, bf16 [B, Hq, Sq, D]           written: each element is the
+ *        fp32 value attn_fwd would store, rounded to nearest even
+ *   every other argument, the validation and the status codes as attn_fwd;
+ *   the aliasing check uses the bf16 size of O
+ *
+ * For callers that keep activations in bf16 (the usual next consumer of an
+ * attention output is a bf16 projection); halves the output traffic.
+ */
+ta_status attn_fwd_bf16out(const void *Q, const void *K, const void *V, void *O, float *LSE,
+                           int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal,
+                           float scale, void *stream);
+
+/*
+ * attn_fwd_split — attn_fwd with the key range of every query tile split
+ * over `num_splits` workgroups, for grids too small to fill the GPU (few
+ * heads, short query blocks against long key sequences).
+ *
+ * Each split computes the softmax result of its rows over its own keys,
+ * (O_s, LSE_s), into the workspace; a second kernel merges them exactly:
+ * LSE = log sum_s exp(LSE_s) and O = sum_s exp(LSE_s - LSE) O_s.  This is the
+ * same rescaling the online softmax applies between key tiles, applied
+ * between splits.  Results agree with attn_fwd to within fp32 rounding.
+ *
+ *   O          device, [B, Hq, Sq, D]: fp32, or bf16 if o_bf16 != 0
+ *   num_splits 1..128 requested; splits are whole key tiles, so at most
+ *              ceil(Sk / BN) are launched; 1 runs attn_fwd / attn_fwd_bf16out
+ *              and ignores the workspace
+ *   workspace  device, 16-byte aligned, at least the size
+ *              ta_split_workspace_bytes reports (owned by the caller, which
+ *              may reuse it once the call's work on `stream` has finished;
+ *              its contents on entry do not matter); must not overlap any
+ *              other argument (TA_ERR_ALIASING)
+ *   other arguments, validation and status codes as attn_fwd;
+ *   TA_ERR_WORKSPACE if num_splits > 1 and workspace is NULL or too small
+ */
+ta_status attn_fwd_split(const void *Q, const void *K, const void *V, void *O, int o_bf16,
+                         float *LSE, int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal,
+                         float scale, int num_splits, void *workspace, size_t workspace_bytes,
+                         void *stream);
+
+/* Workspace bytes attn_fwd_split needs: num_splits * B*Hq*Sq * (D + 1) * 4
+ * for num_splits > 1 (fp32 partial O and LSE per split), 0 for 1.
+ * TA_ERR_INVALID_SHAPE / TA_ERR_UNSUPPORTED / TA_ERR_NULL_POINTER as above.
+ * No HIP call. */
+ta_status ta_split_workspace_bytes(int B, int Hq, int Sq, int D, int num_splits,
+                                   size_t *bytes);
+
+/* A split count for attn_fwd_split: 1 when B*Hq*ceil(Sq/BM) workgroups
+ * already give two per CU (512), else enough splits to reach that, keeping
+ * at least 32 key tiles (2048 keys) per split: shorter splits lose more to
+ * the merge kernel's launch and traffic than the extra workgroups win.
+ * No HIP call. */
+ta_status ta_split_heuristic(int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal,
+                             int *num_splits);
 
 /*
  * ta_schedule — host-side tile schedule of attn_fwd, for tests and tools.

@@ -19,14 +19,14 @@
 //    A operand (V^T) is read from the row-major V tile with the gfx950 LDS
 //    transpose read ds_read_b64_tr_b16, so V needs no reshuffle.  The
 //    per-row rescale factor is a per-lane scalar.
-//  * K and V tiles go global -> LDS by direct DMA (global_load_lds_dwordx4,
-//    16 bytes per lane), double-buffered, with one barrier per tile.  Each
-//    lane fetches the 16-byte chunk that belongs at its LDS slot, which is
-//    how the XOR swizzles that keep the MFMA operand reads bank-conflict
-//    free are applied.
-//  * Software pipeline: while the exponentials of tile j are computed on
-//    the VALU, the MFMAs of the scores of tile j+1 run (K is one tile ahead
-//    of V in LDS).
+//  * K and V tiles go global -> LDS by direct DMA (buffer_load_dwordx4 ...
+//    lds, 16 bytes per lane), double-buffered: the DMA of tile j+1 is issued
+//    before the math on tile j, with one barrier per tile.  Each lane
+//    fetches the 16-byte chunk that belongs at its LDS slot, which is how
+//    the XOR swizzles that keep the MFMA operand reads bank-conflict free
+//    are applied.
+//  * Two workgroups share each CU (two waves per SIMD), so the MFMAs of one
+//    wave overlap the softmax arithmetic of the other.
 //  * The running max is only raised when a row's tile max exceeds it by more
 //    than 2^8 (lazy rescaling): until then weights stay <= 2^8 and the
 //    accumulator needs no rescale.  The final result is the same softmax.
@@ -85,10 +85,17 @@ struct Cfg {
 
 struct Args {
     const uint16_t *Q, *K, *V;
-    float *O, *LSE;
+    // O: fp32 or bf16 [B, Hq, Sq, D] (per the kernel's OBF16), LSE fp32
+    // [B, Hq, Sq].  With key splits these are the partial results of split 0
+    // and split s adds s * o_split / s * l_split elements.
+    void *O;
+    float *LSE;
+    size_t o_split, l_split;
     int B, Hq, Hkv, Sq, Sk;
     int group;       // Hq / Hkv
     int n_qt;        // query tiles per head
+    int n_split;     // key-range splits per query tile
+    int split_tiles; // key tiles per split
     int n_wg;        // total workgroups
     float c;         // scale * log2(e)
 };
@@ -121,15 +128,19 @@ __device__ __forceinline__ float sum_halves(float x)
 
 __device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
-// Workgroup id -> (head index b*Hq+h, query tile).  The hardware hands
-// workgroup i to XCD i % 8; give each XCD a contiguous block of logical ids.
-__device__ __forceinline__ void decode_wg(const Args &a, int bid, int &head, int &qt)
+// Workgroup id -> (head index b*Hq+h, query tile, key split).  The hardware
+// hands workgroup i to XCD i % 8; give each XCD a contiguous block of
+// logical ids, ordered head-major so a head's K/V stay in one XCD's L2.
+__device__ __forceinline__ void decode_wg(const Args &a, int bid, int &head, int &qt,
+                                          int &split)
 {
     const int per = a.n_wg / NXCD, rem = a.n_wg % NXCD;
     const int xcd = bid % NXCD, idx = bid / NXCD;
     const int logical = xcd * per + (xcd < rem ? xcd : rem) + idx;
-    head = logical / a.n_qt;
-    qt = logical % a.n_qt;
+    const int per_head = a.n_qt * a.n_split;
+    head = logical / per_head;
+    qt = (logical % per_head) / a.n_split;
+    split = logical % a.n_split;
 }
 
 template <int D, bool CAUSAL>
@@ -237,8 +248,12 @@ struct Kernel {
         const float m_tile = MASKED && mx == -INFINITY ? -INFINITY : mx * a.c;
         // raise the running max only past the slack (wave-uniform decision)
         if (__builtin_amdgcn_ballot_w64(m_tile > m_run + RESCALE_SLACK)) {
+            // (the branch is wave-uniform: a lane whose row has seen no key
+            // yet may have m_run = m_tile = -inf; its alpha is 1, not NaN)
             const float m_new = fmaxf(m_run, m_tile);
-            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 when m_run = -inf
+            const float alpha = m_new == -INFINITY
+                                    ? 1.f
+                                    : __builtin_amdgcn_exp2f(m_run - m_new);  // 0 if m_run = -inf
             m_run = m_new;
             l_run *= alpha;
 #pragma unroll
@@ -319,7 +334,7 @@ struct Kernel {
     }
 };
 
-template <int D, bool CAUSAL>
+template <int D, bool CAUSAL, bool OBF16>
 __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(Args args)
 {
     using C = Cfg<D>;
@@ -338,8 +353,8 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(Args args)
     k.col = k.lane & 31;
     k.half = k.lane >> 5;
 
-    int head, qt;
-    decode_wg(a, blockIdx.x, head, qt);
+    int head, qt, split;
+    decode_wg(a, blockIdx.x, head, qt, split);
     if (CAUSAL)
         qt = a.n_qt - 1 - qt;   // heaviest query tiles of a head first
     const int b = head / a.Hq, hq = head % a.Hq;
@@ -359,6 +374,25 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(Args args)
         n_kv = min(n_kv_all, (q_last_wg + k.off) / BN + 1);
         first_masked = min(first_masked, max(0, (q0 + k.off + 1) / BN));
         first_masked = min(first_masked, n_kv);
+    }
+
+    // this workgroup's key tiles: [j_lo, j_hi) of the visible ones
+    const int j_lo = split * a.split_tiles;
+    const int j_hi = min(n_kv, j_lo + a.split_tiles);
+    const size_t row0 = ((size_t)b * a.Hq + hq) * a.Sq;
+    if (j_lo >= j_hi) {
+        // no visible key of this split: an empty partial result
+        // (LSE = -inf, O = 0), which the combine step weights by zero
+        const int r = q0 + (int)tid / 2;
+        if (tid < 2 * BM && r < a.Sq) {
+            float *op = (float *)a.O + (size_t)split * a.o_split + (row0 + r) * D;
+#pragma unroll
+            for (int d = (tid & 1) * (D / 2); d < (tid & 1) * (D / 2) + D / 2; d += 4)
+                *(float4 *)(op + d) = float4{0.f, 0.f, 0.f, 0.f};
+            if ((tid & 1) == 0)
+                a.LSE[(size_t)split * a.l_split + row0 + r] = -INFINITY;
+        }
+        return;
     }
 
     const size_t kv_base = ((size_t)b * a.Hkv + hk) * (size_t)a.Sk * D;
@@ -391,9 +425,9 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(Args args)
         return wave_has_rows && (!CAUSAL || j * BN <= k.q_last_wave + k.off);
     };
 
-    // prologue: tile 0 in flight
-    k.template dma_tile<false>(0, kb0);
-    k.template dma_tile<true>(0, vb0);
+    // prologue: tile j_lo in flight
+    k.template dma_tile<false>(j_lo, kb0);
+    k.template dma_tile<true>(j_lo, vb0);
     wait_dma();
     __syncthreads();
 
@@ -402,24 +436,26 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(Args args)
     // barrier).  Tiles before first_masked are fully visible to every real
     // query of the workgroup; a wave holding only padding rows (past Sq)
     // computes on zero queries there and never stores.
-    int j = 0;
-    for (; j + 1 < first_masked; j += 2) {
-        k.fast_step(j, n_kv, kb0, kb1, vb0, vb1);
-        k.fast_step(j + 1, n_kv, kb1, kb0, vb1, vb0);
+    // (buffer parity counts from j_lo)
+    const int j_fast = min(first_masked, j_hi);
+    int j = j_lo;
+    for (; j + 1 < j_fast; j += 2) {
+        k.fast_step(j, j_hi, kb0, kb1, vb0, vb1);
+        k.fast_step(j + 1, j_hi, kb1, kb0, vb1, vb0);
     }
-    if (j < first_masked) {
-        k.fast_step(j, n_kv, kb0, kb1, vb0, vb1);
+    if (j < j_fast) {
+        k.fast_step(j, j_hi, kb0, kb1, vb0, vb1);
         ++j;
     }
 
     // Remaining tiles (masked): waves skip tiles they cannot see.
-    for (; j < n_kv; ++j) {
-        const bool odd = j & 1;
+    for (; j < j_hi; ++j) {
+        const bool odd = (j - j_lo) & 1;
         const unsigned char *kc = odd ? kb1 : kb0;
         unsigned char *kn = odd ? kb0 : kb1;
         const unsigned char *vc = odd ? vb1 : vb0;
         unsigned char *vn = odd ? vb0 : vb1;
-        if (j + 1 < n_kv) {
+        if (j + 1 < j_hi) {
             k.template dma_tile<false>(j + 1, kn);
             k.template dma_tile<true>(j + 1, vn);
         }
@@ -433,31 +469,92 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(Args args)
         __syncthreads();
     }
 
-    // epilogue: normalise, store O rows and LSE
+    // epilogue: normalise, store O rows (fp32, or bf16 rounded to nearest
+    // even) and LSE.  A row that saw no key of its split (only possible with
+    // key splits) stores the empty partial result: O = 0, LSE = -inf.
     const float l = sum_halves(k.l_run);
     if (k.qi < a.Sq) {
-        const float inv = 1.f / l;
-        float *op = a.O + (((size_t)b * a.Hq + hq) * a.Sq + k.qi) * D;
+        const bool empty = !(l > 0.f);
+        const float inv = empty ? 0.f : 1.f / l;
+        const size_t row = row0 + k.qi;
 #pragma unroll
         for (int db = 0; db < C::DB; ++db)
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                float4 v;
-                v.x = k.acc_o[db][4 * g + 0] * inv;
-                v.y = k.acc_o[db][4 * g + 1] * inv;
-                v.z = k.acc_o[db][4 * g + 2] * inv;
-                v.w = k.acc_o[db][4 * g + 3] * inv;
-                *(float4 *)(op + 32 * db + 8 * g + 4 * k.half) = v;
+                const int d = 32 * db + 8 * g + 4 * k.half;
+                const float x0 = k.acc_o[db][4 * g + 0] * inv, x1 = k.acc_o[db][4 * g + 1] * inv;
+                const float x2 = k.acc_o[db][4 * g + 2] * inv, x3 = k.acc_o[db][4 * g + 3] * inv;
+                if (OBF16) {
+                    const u32x2 v = {pack_bf16(x0, x1), pack_bf16(x2, x3)};
+                    *(u32x2 *)((uint16_t *)a.O + row * D + d) = v;
+                } else {
+                    *(float4 *)((float *)a.O + (size_t)split * a.o_split + row * D + d) =
+                        float4{x0, x1, x2, x3};
+                }
             }
         if (k.half == 0)
-            a.LSE[((size_t)b * a.Hq + hq) * a.Sq + k.qi] = (k.m_run + log2f(l)) * LN2;
+            a.LSE[(size_t)split * a.l_split + row] =
+                empty ? -INFINITY : (k.m_run + log2f(l)) * LN2;
     }
 }
 
-template <int D, bool CAUSAL>
+template <int D, bool CAUSAL, bool OBF16>
 hipError_t launch(const Args &a, hipStream_t stream)
 {
-    hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL>), dim3(a.n_wg), dim3(NT), 0, stream, a);
+    hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, OBF16>), dim3(a.n_wg), dim3(NT), 0, stream, a);
+    return hipGetLastError();
+}
+
+// Merge the partial results of the key splits of every row:
+//   LSE = log sum_s exp(LSE_s),  O = sum_s exp(LSE_s - LSE) O_s,
+// where (O_s, LSE_s) is the softmax result over the keys of split s alone
+// (LSE_s = -inf, O_s = 0 for a split without a visible key).  D/4 threads
+// per row, 4 consecutive elements each.
+template <int D, bool OBF16>
+__global__ __launch_bounds__(256) void combine_kernel(const float *Op, const float *Lp, void *O,
+                                                      float *LSE, int n_rows, int n_split,
+                                                      size_t o_split, size_t l_split)
+{
+    constexpr int TPR = D / 4;
+    constexpr int RPB = 256 / TPR;
+    const int t = threadIdx.x % TPR;
+    const int row = blockIdx.x * RPB + threadIdx.x / TPR;
+    if (row >= n_rows)
+        return;
+    float m = -INFINITY;
+    for (int s = 0; s < n_split; ++s)
+        m = fmaxf(m, Lp[s * l_split + row]);
+    float4 acc = {0.f, 0.f, 0.f, 0.f};
+    float wsum = 0.f;
+    for (int s = 0; s < n_split; ++s) {
+        const float ls = Lp[s * l_split + row];
+        const float w = ls == -INFINITY ? 0.f : expf(ls - m);
+        const float4 o = *(const float4 *)(Op + s * o_split + (size_t)row * D + 4 * t);
+        acc.x += w * o.x;
+        acc.y += w * o.y;
+        acc.z += w * o.z;
+        acc.w += w * o.w;
+        wsum += w;
+    }
+    const float inv = 1.f / wsum;
+    const float x0 = acc.x * inv, x1 = acc.y * inv, x2 = acc.z * inv, x3 = acc.w * inv;
+    if (OBF16) {
+        const u32x2 v = {pack_bf16(x0, x1), pack_bf16(x2, x3)};
+        *(u32x2 *)((uint16_t *)O + (size_t)row * D + 4 * t) = v;
+    } else {
+        *(float4 *)((float *)O + (size_t)row * D + 4 * t) = float4{x0, x1, x2, x3};
+    }
+    if (t == 0)
+        LSE[row] = m + logf(wsum);
+}
+
+template <int D, bool OBF16>
+hipError_t launch_combine(const float *Op, const float *Lp, void *O, float *LSE, int n_rows,
+                          int n_split, size_t o_split, size_t l_split, hipStream_t stream)
+{
+    constexpr int RPB = 256 / (D / 4);
+    hipLaunchKernelGGL((combine_kernel<D, OBF16>), dim3((n_rows + RPB - 1) / RPB), dim3(256), 0,
+                       stream, Op, Lp, O, LSE, n_rows, n_split, o_split, l_split);
     return hipGetLastError();
 }
 
@@ -491,12 +588,36 @@ void schedule(int Sq, int Sk, int causal, int qt, int *n_kv, int *first_masked)
     *first_masked = fm;
 }
 
-}  // namespace
+constexpr int MAX_SPLITS = 128;
+// split heuristic: aim for two resident workgroups per CU (256 CUs), with at
+// least 32 key tiles (2048 keys) per split, so that the work of a split
+// outweighs the second launch and the partial-result traffic of the merge
+constexpr int64_t SPLIT_TARGET_WG = 512;
+constexpr int SPLIT_MIN_TILES = 32;
 
-extern "C" {
+// Key tiles per split and the number of splits actually launched for a
+// requested split count (trailing splits that would start past the last key
+// tile are dropped).
+void split_shape(int Sk, int num_splits, int *split_tiles, int *n_split)
+{
+    const int n_kv_all = (Sk + BN - 1) / BN;
+    const int per = (n_kv_all + num_splits - 1) / num_splits;
+    *split_tiles = per;
+    *n_split = (n_kv_all + per - 1) / per;
+}
 
-ta_status attn_fwd(const void *Q, const void *K, const void *V, float *O, float *LSE, int B,
-                   int Hq, int Hkv, int Sq, int Sk, int D, int causal, float scale, void *stream)
+size_t split_workspace_bytes(int B, int Hq, int Sq, int D, int num_splits)
+{
+    const size_t rows = (size_t)B * Hq * Sq;
+    return (size_t)num_splits * rows * (size_t)(D + 1) * 4;
+}
+
+// Validation and launch shared by every entry point.  num_splits == 1 runs
+// one kernel writing O and LSE; num_splits > 1 writes per-split partial
+// results into the workspace and merges them with combine_kernel.
+ta_status attn_fwd_any(const void *Q, const void *K, const void *V, void *O, bool o_bf16,
+                       float *LSE, int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal,
+                       float scale, int num_splits, void *ws, size_t ws_bytes, void *stream)
 {
     if (!Q || !K || !V || !O || !LSE)
         return TA_ERR_NULL_POINTER;
@@ -504,33 +625,48 @@ ta_status attn_fwd(const void *Q, const void *K, const void *V, float *O, float 
         return TA_ERR_INVALID_SHAPE;
     if (Hq % Hkv != 0 || (causal && Sq > Sk))
         return TA_ERR_INVALID_SHAPE;
+    if (num_splits < 1 || num_splits > MAX_SPLITS)
+        return TA_ERR_INVALID_SHAPE;
     if (D != 64 && D != 128)
         return TA_ERR_UNSUPPORTED;
+    int split_tiles, n_split;
+    split_shape(Sk, num_splits, &split_tiles, &n_split);
     // 32-bit in-kernel offsets are used within one (batch, head) slice only;
     // the grid itself must fit a 32-bit workgroup count
     const int64_t n_qt = ((int64_t)Sq + BM - 1) / BM;
-    const int64_t n_wg = (int64_t)B * Hq * n_qt;
-    if ((int64_t)Sq * D >= (1ll << 31) || (int64_t)Sk * D >= (1ll << 31) || n_wg >= (1ll << 31))
+    const int64_t n_wg = (int64_t)B * Hq * n_qt * n_split;
+    const int64_t n_rows = (int64_t)B * Hq * Sq;
+    if ((int64_t)Sq * D >= (1ll << 31) || (int64_t)Sk * D >= (1ll << 31) ||
+        n_wg >= (1ll << 31) || n_rows >= (1ll << 31))
         return TA_ERR_INVALID_SHAPE;
     if (misaligned(Q) || misaligned(K) || misaligned(V) || misaligned(O) || misaligned(LSE))
         return TA_ERR_MISALIGNED;
     if (!(scale >= 0.f) || !isfinite(scale))
         return TA_ERR_INVALID_SCALE;
     const size_t nq = (size_t)B * Hq * Sq * D, nkv = (size_t)B * Hkv * Sk * D;
-    const size_t nl = (size_t)B * Hq * Sq;
-    const size_t o_bytes = nq * 4, l_bytes = nl * 4;
+    const size_t nl = (size_t)n_rows;
+    const size_t o_bytes = nq * (o_bf16 ? 2 : 4), l_bytes = nl * 4;
     if (overlaps(O, o_bytes, Q, nq * 2) || overlaps(O, o_bytes, K, nkv * 2) ||
         overlaps(O, o_bytes, V, nkv * 2) || overlaps(LSE, l_bytes, Q, nq * 2) ||
         overlaps(LSE, l_bytes, K, nkv * 2) || overlaps(LSE, l_bytes, V, nkv * 2) ||
         overlaps(O, o_bytes, LSE, l_bytes))
         return TA_ERR_ALIASING;
+    const size_t need = n_split > 1 ? split_workspace_bytes(B, Hq, Sq, D, n_split) : 0;
+    if (n_split > 1) {
+        if (!ws || ws_bytes < need)
+            return TA_ERR_WORKSPACE;
+        if (misaligned(ws))
+            return TA_ERR_MISALIGNED;
+        if (overlaps(ws, need, Q, nq * 2) || overlaps(ws, need, K, nkv * 2) ||
+            overlaps(ws, need, V, nkv * 2) || overlaps(ws, need, O, o_bytes) ||
+            overlaps(ws, need, LSE, l_bytes))
+            return TA_ERR_ALIASING;
+    }
 
     Args a;
     a.Q = (const uint16_t *)Q;
     a.K = (const uint16_t *)K;
     a.V = (const uint16_t *)V;
-    a.O = O;
-    a.LSE = LSE;
     a.B = B;
     a.Hq = Hq;
     a.Hkv = Hkv;
@@ -538,16 +674,109 @@ ta_status attn_fwd(const void *Q, const void *K, const void *V, float *O, float 
     a.Sk = Sk;
     a.group = Hq / Hkv;
     a.n_qt = (int)n_qt;
+    a.n_split = n_split;
+    a.split_tiles = split_tiles;
     a.n_wg = (int)n_wg;
     a.c = scale * LOG2E;
+    float *Op = (float *)ws, *Lp = Op + (size_t)n_split * nq;
+    if (n_split > 1) {
+        a.O = Op;
+        a.LSE = Lp;
+        a.o_split = nq;
+        a.l_split = nl;
+    } else {
+        a.O = O;
+        a.LSE = LSE;
+        a.o_split = 0;
+        a.l_split = 0;
+    }
 
     hipStream_t s = (hipStream_t)stream;
     hipError_t e;
-    if (D == 64)
-        e = causal ? launch<64, true>(a, s) : launch<64, false>(a, s);
-    else
-        e = causal ? launch<128, true>(a, s) : launch<128, false>(a, s);
+    const bool kb = o_bf16 && n_split == 1;   // the attention kernel writes bf16 O itself
+    if (kb) {
+        if (D == 64)
+            e = causal ? launch<64, true, true>(a, s) : launch<64, false, true>(a, s);
+        else
+            e = causal ? launch<128, true, true>(a, s) : launch<128, false, true>(a, s);
+    } else {
+        if (D == 64)
+            e = causal ? launch<64, true, false>(a, s) : launch<64, false, false>(a, s);
+        else
+            e = causal ? launch<128, true, false>(a, s) : launch<128, false, false>(a, s);
+    }
+    if (e == hipSuccess && n_split > 1) {
+        const int nr = (int)n_rows;
+        if (D == 64)
+            e = o_bf16 ? launch_combine<64, true>(Op, Lp, O, LSE, nr, n_split, nq, nl, s)
+                       : launch_combine<64, false>(Op, Lp, O, LSE, nr, n_split, nq, nl, s);
+        else
+            e = o_bf16 ? launch_combine<128, true>(Op, Lp, O, LSE, nr, n_split, nq, nl, s)
+                       : launch_combine<128, false>(Op, Lp, O, LSE, nr, n_split, nq, nl, s);
+    }
     return e == hipSuccess ? TA_OK : TA_ERR_LAUNCH;
+}
+
+}  // namespace
+
+extern "C" {
+
+ta_status attn_fwd(const void *Q, const void *K, const void *V, float *O, float *LSE, int B,
+                   int Hq, int Hkv, int Sq, int Sk, int D, int causal, float scale, void *stream)
+{
+    return attn_fwd_any(Q, K, V, O, false, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale, 1, nullptr,
+                        0, stream);
+}
+
+ta_status attn_fwd_bf16out(const void *Q, const void *K, const void *V, void *O, float *LSE,
+                           int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal,
+                           float scale, void *stream)
+{
+    return attn_fwd_any(Q, K, V, O, true, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale, 1, nullptr,
+                        0, stream);
+}
+
+ta_status attn_fwd_split(const void *Q, const void *K, const void *V, void *O, int o_bf16,
+                         float *LSE, int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal,
+                         float scale, int num_splits, void *workspace, size_t workspace_bytes,
+                         void *stream)
+{
+    return attn_fwd_any(Q, K, V, O, o_bf16 != 0, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale,
+                        num_splits, workspace, workspace_bytes, stream);
+}
+
+ta_status ta_split_workspace_bytes(int B, int Hq, int Sq, int D, int num_splits, size_t *bytes)
+{
+    if (!bytes)
+        return TA_ERR_NULL_POINTER;
+    if (B < 1 || Hq < 1 || Sq < 1 || num_splits < 1 || num_splits > MAX_SPLITS)
+        return TA_ERR_INVALID_SHAPE;
+    if (D != 64 && D != 128)
+        return TA_ERR_UNSUPPORTED;
+    *bytes = num_splits > 1 ? split_workspace_bytes(B, Hq, Sq, D, num_splits) : 0;
+    return TA_OK;
+}
+
+ta_status ta_split_heuristic(int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal,
+                             int *num_splits)
+{
+    if (!num_splits)
+        return TA_ERR_NULL_POINTER;
+    if (B < 1 || Hq < 1 || Hkv < 1 || Sq < 1 || Sk < 1 || Hq % Hkv != 0 || (causal && Sq > Sk))
+        return TA_ERR_INVALID_SHAPE;
+    if (D != 64 && D != 128)
+        return TA_ERR_UNSUPPORTED;
+    const int64_t n_wg = (int64_t)B * Hq * (((int64_t)Sq + BM - 1) / BM);
+    const int n_kv_all = (Sk + BN - 1) / BN;
+    int n = 1;
+    if (n_wg < SPLIT_TARGET_WG) {
+        n = (int)((SPLIT_TARGET_WG + n_wg - 1) / n_wg);
+        n = n < n_kv_all / SPLIT_MIN_TILES ? n : n_kv_all / SPLIT_MIN_TILES;
+        n = n < MAX_SPLITS ? n : MAX_SPLITS;
+        n = n > 1 ? n : 1;
+    }
+    *num_splits = n;
+    return TA_OK;
 }
 
 ta_status ta_schedule(int Sq, int Sk, int D, int causal, int q_tile, int *n_kv_tiles,
@@ -587,10 +816,11 @@ const char *ta_status_string(ta_status s)
     case TA_ERR_INVALID_SCALE: return "scale must be finite and >= 0";
     case TA_ERR_ALIASING: return "output overlaps an input or the other output";
     case TA_ERR_LAUNCH: return "HIP launch error";
+    case TA_ERR_WORKSPACE: return "split workspace missing or too small";
     }
     return "unknown status";
 }
 
-int ta_version(void) { return 200; }
+int ta_version(void) { return 300; }
 
 }  // extern "C"

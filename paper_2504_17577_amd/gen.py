@@ -55,12 +55,12 @@ class Workload:
         PV each cost 2*D flops per visible pair."""
         return 4 * self.D * self.B * self.Hq * self.pairs()
 
-    def bytes(self) -> int:
-        """Algorithmic HBM bytes: bf16 Q, K, V read once, fp32 O and LSE
-        written once."""
+    def bytes(self, o_bytes: int = 4) -> int:
+        """Algorithmic HBM bytes: bf16 Q, K, V read once, O (``o_bytes`` per
+        element: 4 for fp32, 2 for bf16) and fp32 LSE written once."""
         q = self.B * self.Hq * self.Sq * self.D
         kv = self.B * self.Hkv * self.Sk * self.D
-        return 2 * (q + 2 * kv) + 4 * q + 4 * self.B * self.Hq * self.Sq
+        return 2 * (q + 2 * kv) + o_bytes * q + 4 * self.B * self.Hq * self.Sq
 
     def describe(self) -> str:
         s = (f"B={self.B} Hq={self.Hq} Hkv={self.Hkv} Sq={self.Sq} Sk={self.Sk} "
@@ -72,7 +72,8 @@ class Workload:
 
 # Workloads: a tiny correctness case, a causal D=64 case, the dense D=128
 # throughput case, a long causal case with peaky keys, a grouped-query causal
-# case, and the paper's five FlashAttention benchmark shapes.  All draw Q/K/V
+# case, the paper's five FlashAttention benchmark shapes, and two shapes with
+# fewer queries than keys.  All draw Q/K/V
 # i.i.d. N(0,1) in bf16 with scale 1/sqrt(D).
 WORKLOADS = {
     w.name: w
@@ -90,6 +91,11 @@ WORKLOADS = {
         Workload("paper_fa2_s1k_causal", 12, 1, 32, 32, 1024, 1024, 128, True),
         Workload("paper_fa3_s1k", 13, 1, 32, 32, 1024, 1024, 128, False),
         Workload("paper_fa4_s4k_causal", 14, 1, 32, 32, 4096, 4096, 128, True),
+        # query and key lengths that differ: a 1k-query chunk of a causal
+        # prefill against an 8k-key cache (bottom-right alignment, GQA 4), and
+        # 512 queries attending to 4k keys without a mask
+        Workload("chunk_causal_d128_q1k_k8k", 20, 1, 32, 8, 1024, 8192, 128, True),
+        Workload("cross_d128_q512_k4k", 21, 4, 16, 16, 512, 4096, 128, False),
     )
 }
 

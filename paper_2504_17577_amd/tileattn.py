@@ -17,6 +17,7 @@ TA_OK = 0
 STATUS = {
     0: "TA_OK", 1: "TA_ERR_NULL_POINTER", 2: "TA_ERR_INVALID_SHAPE", 3: "TA_ERR_UNSUPPORTED",
     4: "TA_ERR_MISALIGNED", 5: "TA_ERR_INVALID_SCALE", 6: "TA_ERR_ALIASING", 7: "TA_ERR_LAUNCH",
+    8: "TA_ERR_WORKSPACE",
 }
 
 _lib = None
@@ -40,6 +41,15 @@ def lib():
     p, i = ctypes.c_void_p, ctypes.c_int
     L.attn_fwd.restype = i
     L.attn_fwd.argtypes = [p, p, p, p, p, i, i, i, i, i, i, i, ctypes.c_float, p]
+    L.attn_fwd_bf16out.restype = i
+    L.attn_fwd_bf16out.argtypes = [p, p, p, p, p, i, i, i, i, i, i, i, ctypes.c_float, p]
+    L.attn_fwd_split.restype = i
+    L.attn_fwd_split.argtypes = [p, p, p, p, i, p, i, i, i, i, i, i, i, ctypes.c_float, i, p,
+                                 ctypes.c_size_t, p]
+    L.ta_split_workspace_bytes.restype = i
+    L.ta_split_workspace_bytes.argtypes = [i, i, i, i, i, ctypes.POINTER(ctypes.c_size_t)]
+    L.ta_split_heuristic.restype = i
+    L.ta_split_heuristic.argtypes = [i, i, i, i, i, i, i, ctypes.POINTER(i)]
     L.ta_schedule.restype = i
     L.ta_schedule.argtypes = [i, i, i, i, i, ctypes.POINTER(i), ctypes.POINTER(i)]
     L.ta_tile_shape.restype = i
@@ -77,17 +87,42 @@ def ta_schedule(Sq: int, Sk: int, D: int, causal: bool, q_tile: int):
     return n.value, fm.value
 
 
+def ta_split_workspace_bytes(B: int, Hq: int, Sq: int, D: int, num_splits: int) -> int:
+    n = ctypes.c_size_t()
+    rc = lib().ta_split_workspace_bytes(B, Hq, Sq, D, num_splits, ctypes.byref(n))
+    if rc != TA_OK:
+        raise TileAttnError(rc, ta_status_string(rc))
+    return n.value
+
+
+def ta_split_heuristic(B: int, Hq: int, Hkv: int, Sq: int, Sk: int, D: int, causal: bool) -> int:
+    n = ctypes.c_int()
+    rc = lib().ta_split_heuristic(B, Hq, Hkv, Sq, Sk, D, int(bool(causal)), ctypes.byref(n))
+    if rc != TA_OK:
+        raise TileAttnError(rc, ta_status_string(rc))
+    return n.value
+
+
+def attn_fwd_split_raw(Q, K, V, O, o_bf16, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale,
+                       num_splits, workspace, workspace_bytes, stream) -> int:
+    """attn_fwd_split with integer pointers; returns the status code."""
+    return lib().attn_fwd_split(Q, K, V, O, int(bool(o_bf16)), LSE, B, Hq, Hkv, Sq, Sk, D,
+                                int(causal), float(scale), int(num_splits), workspace,
+                                int(workspace_bytes), stream)
+
+
 def attn_fwd_raw(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale, stream) -> int:
     """The C call with integer pointers; returns the status code."""
     return lib().attn_fwd(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, D, int(causal), float(scale), stream)
 
 
-def attn_fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse=None,
-             stream=None):
-    """O, LSE = attention forward of bf16 BHSD tensors q [B,Hq,Sq,D] and
-    k, v [B,Hkv,Sk,D] on the GPU.  Returns fp32 O [B,Hq,Sq,D] and
-    LSE [B,Hq,Sq].  ``scale`` defaults to 1/sqrt(D).  The launch is
-    asynchronous on ``stream`` (default: torch's current stream)."""
+def attn_fwd_bf16out_raw(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale, stream) -> int:
+    """attn_fwd_bf16out with integer pointers; returns the status code."""
+    return lib().attn_fwd_bf16out(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, D, int(causal),
+                                  float(scale), stream)
+
+
+def _attn(q, k, v, causal, scale, out, lse, stream, o_dtype, raw):
     import torch
 
     for name, t in (("q", q), ("k", k), ("v", v)):
@@ -101,16 +136,69 @@ def attn_fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     if out is None:
-        out = torch.empty((B, Hq, Sq, D), dtype=torch.float32, device=q.device)
+        out = torch.empty((B, Hq, Sq, D), dtype=o_dtype, device=q.device)
     if lse is None:
         lse = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device)
-    for name, t, shape in (("out", out, (B, Hq, Sq, D)), ("lse", lse, (B, Hq, Sq))):
-        if t.dtype != torch.float32 or tuple(t.shape) != shape or not t.is_contiguous():
-            raise TypeError(f"{name} must be a contiguous float32 tensor of shape {shape}")
+    for name, t, shape, dt in (("out", out, (B, Hq, Sq, D), o_dtype),
+                               ("lse", lse, (B, Hq, Sq), torch.float32)):
+        if t.dtype != dt or tuple(t.shape) != shape or not t.is_contiguous():
+            raise TypeError(f"{name} must be a contiguous {dt} tensor of shape {shape}")
     if stream is None:
         stream = torch.cuda.current_stream(q.device)
-    rc = attn_fwd_raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
-                      B, Hq, Hkv, Sq, Sk, D, causal, scale, stream.cuda_stream)
+    rc = raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
+             B, Hq, Hkv, Sq, Sk, D, causal, scale, stream.cuda_stream)
     if rc != TA_OK:
         raise TileAttnError(rc, ta_status_string(rc))
     return out, lse
+
+
+def attn_fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse=None,
+             stream=None):
+    """O, LSE = attention forward of bf16 BHSD tensors q [B,Hq,Sq,D] and
+    k, v [B,Hkv,Sk,D] on the GPU.  Returns fp32 O [B,Hq,Sq,D] and
+    LSE [B,Hq,Sq].  ``scale`` defaults to 1/sqrt(D).  The launch is
+    asynchronous on ``stream`` (default: torch's current stream)."""
+    import torch
+
+    return _attn(q, k, v, causal, scale, out, lse, stream, torch.float32, attn_fwd_raw)
+
+
+def attn_fwd_bf16out(q, k, v, causal: bool = False, scale: float | None = None, out=None,
+                     lse=None, stream=None):
+    """As attn_fwd, with O returned in bfloat16 (the fp32 result rounded to
+    nearest even by the kernel)."""
+    import torch
+
+    return _attn(q, k, v, causal, scale, out, lse, stream, torch.bfloat16, attn_fwd_bf16out_raw)
+
+
+def attn_fwd_split(q, k, v, causal: bool = False, scale: float | None = None,
+                   num_splits: int | None = None, out=None, lse=None, workspace=None,
+                   out_dtype=None, stream=None):
+    """attn_fwd with the key range split over ``num_splits`` workgroups per
+    query tile (default: ta_split_heuristic) and the partial results merged
+    by a second kernel.  ``workspace`` is a uint8 GPU tensor of at least
+    ta_split_workspace_bytes(...) bytes (allocated here if None); it must
+    stay alive until the launch has finished on ``stream``.  ``out_dtype``
+    is torch.float32 (default) or torch.bfloat16."""
+    import torch
+
+    o_dtype = torch.float32 if out_dtype is None else out_dtype
+    if o_dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("out_dtype must be torch.float32 or torch.bfloat16")
+    B, Hq, Sq, D = q.shape
+    Hkv, Sk = k.shape[1], k.shape[2]
+    if num_splits is None:
+        num_splits = ta_split_heuristic(B, Hq, Hkv, Sq, Sk, D, causal)
+    need = ta_split_workspace_bytes(B, Hq, Sq, D, num_splits)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    if workspace.dtype != torch.uint8 or not workspace.is_cuda or not workspace.is_contiguous():
+        raise TypeError("workspace must be a contiguous uint8 GPU tensor")
+    ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel()
+
+    def raw(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale, stream):
+        return attn_fwd_split_raw(Q, K, V, O, o_dtype == torch.bfloat16, LSE, B, Hq, Hkv, Sq, Sk,
+                                  D, causal, scale, num_splits, ws_ptr, ws_bytes, stream)
+
+    return _attn(q, k, v, causal, scale, out, lse, stream, o_dtype, raw)

@@ -29,8 +29,8 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_strings():
-    assert ta.ta_version() >= 100
-    for s in range(8):
+    assert ta.ta_version() >= 300
+    for s in range(9):
         assert ta.ta_status_string(s)
     assert ta.ta_status_string(99) == "unknown status"
     assert ta.ta_tile_shape(64) == ta.ta_tile_shape(128)
@@ -38,8 +38,12 @@ def test_version_and_strings():
         ta.ta_tile_shape(96)
 
 
-# Fake, 16-byte aligned, non-overlapping addresses: every call below fails
-# validation, so nothing is ever dereferenced or launched.
+# Fake, 16-byte aligned, non-overlapping addresses: every call below must
+# fail validation, so nothing is ever dereferenced or launched.  A wrong
+# expectation in this table would launch a kernel on these addresses, so the
+# fake-pointer tests run only where no GPU is present (no /dev/kfd).
+no_gpu = pytest.mark.skipif(os.path.exists("/dev/kfd"),
+                            reason="fake-pointer validation cases run only without a GPU")
 Q, K, V, O, L = 0x10000000, 0x20000000, 0x30000000, 0x40000000, 0x50000000
 OK = dict(Q=Q, K=K, V=V, O=O, LSE=L, B=1, Hq=2, Hkv=2, Sq=128, Sk=128, D=64, causal=0,
           scale=0.125, stream=None)
@@ -56,6 +60,7 @@ BAD = [
 ]
 
 
+@no_gpu
 @pytest.mark.parametrize("change,status", BAD, ids=[str(c) for c, _ in BAD])
 def test_validation_before_any_hip_call(change, status):
     a = dict(OK, **change)
@@ -101,3 +106,71 @@ def test_schedule_matches_brute_force(D):
             assert total == want
     with pytest.raises(ta.TileAttnError):
         ta.ta_schedule(100, 100, D, False, 1)   # only one query tile
+
+
+# attn_fwd_split: the same argument errors, plus the split count and the
+# workspace.  Sk=128 is two key tiles, so two splits really split and the
+# workspace is checked; a fake workspace far from every other buffer.
+WS = 0x60000000
+WS_OK = dict(OK, splits=2, ws=WS, ws_bytes=1 << 24, o_bf16=0)
+BAD_SPLIT = [(c, st) for c, st in BAD] + [
+    (dict(splits=0), 2), (dict(splits=129), 2), (dict(splits=-1), 2),
+    (dict(ws=0), 8), (dict(ws_bytes=2 * 2 * 128 * 65 * 4 - 1), 8),
+    (dict(ws=WS + 8), 4), (dict(ws=Q - 4096), 6), (dict(ws=O + 4096), 6),
+    (dict(ws=L - 16), 6), (dict(o_bf16=1, O=L - 2 * 128 * 64 * 2 + 16), 6),
+]
+
+
+@no_gpu
+@pytest.mark.parametrize("change,status", BAD_SPLIT, ids=[str(c) for c, _ in BAD_SPLIT])
+def test_split_validation_before_any_hip_call(change, status):
+    a = dict(WS_OK, **change)
+    rc = ta.attn_fwd_split_raw(a["Q"], a["K"], a["V"], a["O"], a["o_bf16"], a["LSE"], a["B"],
+                               a["Hq"], a["Hkv"], a["Sq"], a["Sk"], a["D"], a["causal"],
+                               a["scale"], a["splits"], a["ws"], a["ws_bytes"], a["stream"])
+    assert rc == status, f"{change}: got {ta.STATUS.get(rc, rc)}, want {ta.STATUS[status]}"
+
+
+@no_gpu
+def test_bf16out_validation_before_any_hip_call():
+    for change, status in BAD:
+        a = dict(OK, **change)
+        rc = ta.attn_fwd_bf16out_raw(a["Q"], a["K"], a["V"], a["O"], a["LSE"], a["B"], a["Hq"],
+                                     a["Hkv"], a["Sq"], a["Sk"], a["D"], a["causal"], a["scale"],
+                                     a["stream"])
+        assert rc == status, f"{change}: got {ta.STATUS.get(rc, rc)}"
+
+
+def test_split_workspace_bytes():
+    for B, Hq, Sq, D, n in [(1, 2, 128, 64, 2), (3, 5, 77, 128, 7), (1, 32, 1024, 128, 128)]:
+        assert ta.ta_split_workspace_bytes(B, Hq, Sq, D, n) == n * B * Hq * Sq * (D + 1) * 4
+    assert ta.ta_split_workspace_bytes(2, 2, 100, 64, 1) == 0
+    for bad in [(0, 1, 1, 64, 2), (1, 1, 1, 64, 0), (1, 1, 1, 64, 129)]:
+        with pytest.raises(ta.TileAttnError):
+            ta.ta_split_workspace_bytes(*bad)
+    with pytest.raises(ta.TileAttnError):
+        ta.ta_split_workspace_bytes(1, 1, 1, 96, 2)
+
+
+@pytest.mark.parametrize("shape", [
+    (1, 32, 32, 512, 512, 128, True), (1, 32, 32, 512, 512, 128, False),
+    (1, 32, 32, 1024, 1024, 128, True), (1, 32, 32, 4096, 4096, 128, True),
+    (1, 32, 8, 1024, 8192, 128, True), (4, 16, 16, 512, 4096, 128, False),
+    (8, 32, 32, 2048, 2048, 128, False), (1, 2, 2, 128, 128, 64, False),
+    (1, 1, 1, 1, 100000, 64, False), (1, 1, 1, 1, 1, 128, True),
+    (2, 8, 8, 128, 16384, 128, False),
+])
+def test_split_heuristic_properties(shape):
+    B, Hq, Hkv, Sq, Sk, D, causal = shape
+    BM, BN = ta.ta_tile_shape(D)
+    wg = B * Hq * -(-Sq // BM)
+    n_kv = -(-Sk // BN)
+    n = ta.ta_split_heuristic(*shape)
+    assert 1 <= n <= 128
+    if wg >= 512:
+        assert n == 1
+    elif n > 1:
+        assert n <= n_kv // 32                    # at least 32 key tiles per split
+        assert (n - 1) * wg < 512                 # no more splits than the target needs
+    if n == 1 and wg < 512:
+        assert n_kv // 32 <= 1                    # only when the keys are too short to split

@@ -80,7 +80,8 @@ def sample_rows(w, rng, n_random):
 
 @pytest.mark.parametrize("name", ["dense_d128_s2k", "causal_peaky_d128_s8k", "gqa4_causal_d128_s4k",
                                   "paper_fa0_s512_causal", "paper_fa1_s512", "paper_fa2_s1k_causal",
-                                  "paper_fa3_s1k", "paper_fa4_s4k_causal"])
+                                  "paper_fa3_s1k", "paper_fa4_s4k_causal",
+                                  "chunk_causal_d128_q1k_k8k", "cross_d128_q512_k4k"])
 def test_workload_full_size_sampled(ta, name):
     """Full-size workload, in the launch configuration the bench times:
     sampled rows against the oracle, plus properties over every row."""
