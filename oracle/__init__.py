@@ -103,3 +103,49 @@ def attn_rows(q, k, v, causal: bool, scale: float, rows, nthreads: int | None = 
     if rc:
         raise OracleError(f"oracle_attn_rows returned {rc}")
     return o, lse
+
+
+# ---------------------------------------------------------------------------
+# MLA decode (the paper's appendix listing "Implementation of FlashMLA with
+# TileLang"): for batch b and query head h, with latent head
+# hk = h // (H / Hkv),
+#   s_t = scale * (q[b,h] . kv[b,t,hk] + q_pe[b,h] . k_pe[b,t,hk])
+#   O[b,h] = sum_t softmax(s)_t kv[b,t,hk],   LSE[b,h] = ln sum_t exp(s_t)
+# over all Skv cache positions (a decode step sees the whole cache).  This is
+# the attention definition above with one query row per head, key
+# [kv | k_pe] (Dl + Dr wide) and value kv.  The reduction below passes the
+# key as the value too, so both share one width, and drops the Dr output
+# columns that the k_pe part of that value adds.
+
+def _mla_bits(q, q_pe, kv, k_pe):
+    arrs = [np.ascontiguousarray(a) for a in (q, q_pe, kv, k_pe)]
+    for a, nd in zip(arrs, (3, 3, 4, 4)):
+        if a.dtype != np.uint16 or a.ndim != nd:
+            raise TypeError("MLA oracle inputs are bfloat16 bit arrays: q, q_pe [B,H,D], "
+                            "kv, k_pe [B,Skv,Hkv,D]")
+    q, q_pe, kv, k_pe = arrs
+    B, H, Dl = q.shape
+    Skv, Hkv = kv.shape[1], kv.shape[2]
+    Dr = q_pe.shape[2]
+    if (q_pe.shape[:2] != (B, H) or kv.shape != (B, Skv, Hkv, Dl)
+            or k_pe.shape != (B, Skv, Hkv, Dr) or H % Hkv):
+        raise OracleError(f"inconsistent MLA shapes q{q.shape} q_pe{q_pe.shape} "
+                          f"kv{kv.shape} k_pe{k_pe.shape}")
+    qf = np.concatenate([q, q_pe], axis=2)[:, :, None, :]                   # [B,H,1,Dl+Dr]
+    kf = np.ascontiguousarray(np.concatenate([kv, k_pe], axis=3).transpose(0, 2, 1, 3))
+    return qf, kf, Dl                                                       # kf [B,Hkv,Skv,Dl+Dr]
+
+
+def mla_decode(q, q_pe, kv, k_pe, scale: float, nthreads: int | None = None, lib=None):
+    """Every (b, h): returns (O [B,H,Dl], LSE [B,H]) as float64."""
+    qf, kf, Dl = _mla_bits(q, q_pe, kv, k_pe)
+    o, lse = attn_fwd(qf, kf, kf, False, scale, nthreads=nthreads, lib=lib)
+    return np.ascontiguousarray(o[:, :, 0, :Dl]), np.ascontiguousarray(lse[:, :, 0])
+
+
+def mla_rows(q, q_pe, kv, k_pe, scale: float, rows, nthreads: int | None = None, lib=None):
+    """Selected heads ``rows`` = [(b, h), ...]: returns (O [n,Dl], LSE [n])."""
+    qf, kf, Dl = _mla_bits(q, q_pe, kv, k_pe)
+    idx = [(int(b), int(h), 0) for b, h in rows]
+    o, lse = attn_rows(qf, kf, kf, False, scale, idx, nthreads=nthreads, lib=lib)
+    return np.ascontiguousarray(o[:, :Dl]), lse

@@ -157,3 +157,77 @@ def random_problem(B, Hq, Hkv, Sq, Sk, D, seed: int, wid: int = 100, std: float 
 def digest(u: np.ndarray) -> str:
     """Short BLAKE2b digest of an array's bytes (records which inputs ran)."""
     return hashlib.blake2b(np.ascontiguousarray(u).view(np.uint8), digest_size=8).hexdigest()
+
+
+# ---------------------------------------------------------------------------
+# Multi-head latent attention (MLA) decode inputs.  One new query token per
+# batch element attends to a cache of Skv positions.  Layouts follow the
+# paper's MLA listing (appendix "Implementation of FlashMLA with TileLang"):
+#   q     [B, H, Dl]         latent part of the query
+#   q_pe  [B, H, Dr]         rotary part of the query
+#   kv    [B, Skv, Hkv, Dl]  latent cache, used both as key and as value
+#   k_pe  [B, Skv, Hkv, Dr]  rotary part of the key
+# The paper gives no sizes; the workloads use DeepSeek-V3's published MLA
+# dimensions (128 query heads, one latent head of 512, rotary part 64).
+
+TENSOR_QPE, TENSOR_KPE = 3, 4
+
+
+@dataclasses.dataclass(frozen=True)
+class MlaWorkload:
+    """One MLA decode problem: shapes and input recipe (i.i.d. N(0,1))."""
+
+    name: str
+    wid: int
+    B: int
+    H: int
+    Hkv: int
+    Skv: int
+    Dl: int = 512
+    Dr: int = 64
+
+    @property
+    def scale(self) -> float:
+        """Softmax scale 1/sqrt(Dl + Dr) (scores then have unit variance),
+        rounded to the fp32 value both sides use."""
+        return float(np.float32(1.0 / math.sqrt(self.Dl + self.Dr)))
+
+    def flops(self) -> int:
+        """Matmul flops: scores over Dl + Dr, then P V over Dl, per (head, key)."""
+        return 2 * self.B * self.H * self.Skv * (self.Dl + self.Dr + self.Dl)
+
+    def bytes(self) -> int:
+        """Algorithmic HBM bytes: bf16 cache (kv, k_pe) and queries read once,
+        fp32 O and LSE written once."""
+        cache = self.B * self.Skv * self.Hkv * (self.Dl + self.Dr) * 2
+        q = self.B * self.H * (self.Dl + self.Dr) * 2
+        return cache + q + self.B * self.H * (self.Dl + 1) * 4
+
+    def describe(self) -> str:
+        return (f"B={self.B} H={self.H} Hkv={self.Hkv} Skv={self.Skv} Dl={self.Dl} "
+                f"Dr={self.Dr} decode")
+
+
+MLA_WORKLOADS = {
+    w.name: w
+    for w in (
+        MlaWorkload("mla_tiny_s200", 30, 2, 128, 1, 200),
+        MlaWorkload("mla_b64_s8k", 31, 64, 128, 1, 8192),
+        MlaWorkload("mla_b128_s4k", 32, 128, 128, 1, 4096),
+        MlaWorkload("mla_gqa2_b8_s2k", 33, 8, 64, 2, 2048),
+    )
+}
+
+
+def make_mla_inputs(w: MlaWorkload, seed: int = 0):
+    """(q, q_pe, kv, k_pe) bfloat16 bit arrays for MLA workload ``w``."""
+    q = normal_bf16((w.B, w.H, w.Dl), seed, w.wid, TENSOR_Q)
+    q_pe = normal_bf16((w.B, w.H, w.Dr), seed, w.wid, TENSOR_QPE)
+    kv = normal_bf16((w.B, w.Skv, w.Hkv, w.Dl), seed, w.wid, TENSOR_K)
+    k_pe = normal_bf16((w.B, w.Skv, w.Hkv, w.Dr), seed, w.wid, TENSOR_KPE)
+    return q, q_pe, kv, k_pe
+
+
+def random_mla_problem(B, H, Hkv, Skv, seed: int, Dl: int = 512, Dr: int = 64, wid: int = 101):
+    """(q, q_pe, kv, k_pe) bfloat16 bits for an ad-hoc MLA shape."""
+    return make_mla_inputs(MlaWorkload("adhoc", wid, B, H, Hkv, Skv, Dl, Dr), seed)
