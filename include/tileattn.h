@@ -131,6 +131,48 @@ ta_status ta_split_heuristic(int B, int Hq, int Hkv, int Sq, int Sk, int D, int 
                              int *num_splits);
 
 /*
+ * mla_decode — multi-head latent attention, one decode step: the
+ * computation of the paper's appendix listing "Implementation of FlashMLA
+ * with TileLang".  For batch b and query head h, with latent head
+ * hk = h / (H / Hkv), over all Skv cache positions t:
+ *   s_t = scale * (Q[b,h,:] . KV[b,t,hk,:] + Q_pe[b,h,:] . K_pe[b,t,hk,:])
+ *   O[b,h,:] = sum_t softmax(s)_t KV[b,t,hk,:]      (the latent cache is the value)
+ *   LSE[b,h] = ln sum_t exp(s_t)
+ *
+ *   Q     device, bf16 [B, H, Dl]             read only
+ *   Q_pe  device, bf16 [B, H, Dr]             read only
+ *   KV    device, bf16 [B, Skv, Hkv, Dl]      read only (the listing's layout)
+ *   K_pe  device, bf16 [B, Skv, Hkv, Dr]      read only
+ *   O     device, fp32 [B, H, Dl]             written
+ *   LSE   device, fp32 [B, H]                 written (natural log, scale included)
+ *   Dl == 512 and Dr == 64 (else TA_ERR_UNSUPPORTED); H % Hkv == 0
+ *   num_splits: 1..128 requested splits of the cache positions (whole tiles
+ *   of 32; trailing empty splits are dropped); for more than one, the
+ *   per-split results go to `workspace` (device, 16-byte aligned, at least
+ *   mla_workspace_bytes(B, H, num_splits) bytes, owned by the caller, no
+ *   overlap with any other argument) and a second kernel merges them;
+ *   num_splits == 1 ignores the workspace
+ *   scale >= 0, finite; every pointer 16-byte aligned; stream as attn_fwd
+ * Status codes as attn_fwd (TA_ERR_WORKSPACE for a missing or small
+ * workspace).  Scores and sums are fp32, the softmax weights bf16 for the
+ * weighted sum of the latent rows.
+ */
+ta_status mla_decode(const void *Q, const void *Q_pe, const void *KV, const void *K_pe,
+                     float *O, float *LSE, int B, int H, int Hkv, int Skv, int Dl, int Dr,
+                     float scale, int num_splits, void *workspace, size_t workspace_bytes,
+                     void *stream);
+
+/* Workspace bytes mla_decode needs: num_splits * B*H * (Dl + 1) * 4 with
+ * Dl = 512 for num_splits > 1, 0 for 1.  No HIP call. */
+ta_status mla_workspace_bytes(int B, int H, int num_splits, size_t *bytes);
+
+/* A split count for mla_decode: enough splits of the cache for one
+ * workgroup per CU (a workgroup covers 64 query heads of one latent head and
+ * fills its CU's registers), keeping at least 8 tiles (256 positions) per
+ * split.  No HIP call. */
+ta_status mla_split_heuristic(int B, int H, int Hkv, int Skv, int *num_splits);
+
+/*
  * ta_schedule — host-side tile schedule of attn_fwd, for tests and tools.
  * For the query tile `q_tile` (rows q_tile*BM .. q_tile*BM+BM-1, BM from
  * ta_tile_shape) it reports how many key tiles of BN keys the kernel visits

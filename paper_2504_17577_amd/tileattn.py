@@ -50,6 +50,13 @@ def lib():
     L.ta_split_workspace_bytes.argtypes = [i, i, i, i, i, ctypes.POINTER(ctypes.c_size_t)]
     L.ta_split_heuristic.restype = i
     L.ta_split_heuristic.argtypes = [i, i, i, i, i, i, i, ctypes.POINTER(i)]
+    L.mla_decode.restype = i
+    L.mla_decode.argtypes = [p, p, p, p, p, p, i, i, i, i, i, i, ctypes.c_float, i, p,
+                             ctypes.c_size_t, p]
+    L.mla_workspace_bytes.restype = i
+    L.mla_workspace_bytes.argtypes = [i, i, i, ctypes.POINTER(ctypes.c_size_t)]
+    L.mla_split_heuristic.restype = i
+    L.mla_split_heuristic.argtypes = [i, i, i, i, ctypes.POINTER(i)]
     L.ta_schedule.restype = i
     L.ta_schedule.argtypes = [i, i, i, i, i, ctypes.POINTER(i), ctypes.POINTER(i)]
     L.ta_tile_shape.restype = i
@@ -202,3 +209,72 @@ def attn_fwd_split(q, k, v, causal: bool = False, scale: float | None = None,
                                   D, causal, scale, num_splits, ws_ptr, ws_bytes, stream)
 
     return _attn(q, k, v, causal, scale, out, lse, stream, o_dtype, raw)
+
+
+def mla_workspace_bytes(B: int, H: int, num_splits: int) -> int:
+    n = ctypes.c_size_t()
+    rc = lib().mla_workspace_bytes(B, H, num_splits, ctypes.byref(n))
+    if rc != TA_OK:
+        raise TileAttnError(rc, ta_status_string(rc))
+    return n.value
+
+
+def mla_split_heuristic(B: int, H: int, Hkv: int, Skv: int) -> int:
+    n = ctypes.c_int()
+    rc = lib().mla_split_heuristic(B, H, Hkv, Skv, ctypes.byref(n))
+    if rc != TA_OK:
+        raise TileAttnError(rc, ta_status_string(rc))
+    return n.value
+
+
+def mla_decode_raw(Q, Q_pe, KV, K_pe, O, LSE, B, H, Hkv, Skv, Dl, Dr, scale, num_splits,
+                   workspace, workspace_bytes, stream) -> int:
+    """mla_decode with integer pointers; returns the status code."""
+    return lib().mla_decode(Q, Q_pe, KV, K_pe, O, LSE, B, H, Hkv, Skv, Dl, Dr, float(scale),
+                            int(num_splits), workspace, int(workspace_bytes), stream)
+
+
+def mla_decode(q, q_pe, kv, k_pe, scale: float | None = None, num_splits: int | None = None,
+               out=None, lse=None, workspace=None, stream=None):
+    """O [B,H,Dl] fp32, LSE [B,H] fp32 = one MLA decode step of bf16 GPU
+    tensors q [B,H,Dl], q_pe [B,H,Dr], kv [B,Skv,Hkv,Dl], k_pe [B,Skv,Hkv,Dr].
+    ``scale`` defaults to 1/sqrt(Dl + Dr); ``num_splits`` to
+    mla_split_heuristic.  ``workspace`` (uint8 GPU tensor) is allocated here
+    if needed and not given; it must stay alive until the launch has
+    finished on ``stream``."""
+    import torch
+
+    for name, t, nd in (("q", q, 3), ("q_pe", q_pe, 3), ("kv", kv, 4), ("k_pe", k_pe, 4)):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or t.dim() != nd or not t.is_contiguous():
+            raise TypeError(f"{name} must be a contiguous {nd}-D bfloat16 GPU tensor")
+    B, H, Dl = q.shape
+    Dr = q_pe.shape[2]
+    Skv, Hkv = kv.shape[1], kv.shape[2]
+    if (tuple(q_pe.shape[:2]) != (B, H) or tuple(kv.shape) != (B, Skv, Hkv, Dl)
+            or tuple(k_pe.shape) != (B, Skv, Hkv, Dr)):
+        raise TileAttnError(2, f"inconsistent shapes q{tuple(q.shape)} q_pe{tuple(q_pe.shape)} "
+                               f"kv{tuple(kv.shape)} k_pe{tuple(k_pe.shape)}")
+    if scale is None:
+        scale = 1.0 / math.sqrt(Dl + Dr)
+    if num_splits is None:
+        num_splits = mla_split_heuristic(B, H, Hkv, Skv)
+    if out is None:
+        out = torch.empty((B, H, Dl), dtype=torch.float32, device=q.device)
+    if lse is None:
+        lse = torch.empty((B, H), dtype=torch.float32, device=q.device)
+    for name, t, shape in (("out", out, (B, H, Dl)), ("lse", lse, (B, H))):
+        if t.dtype != torch.float32 or tuple(t.shape) != shape or not t.is_contiguous():
+            raise TypeError(f"{name} must be a contiguous float32 tensor of shape {shape}")
+    need = mla_workspace_bytes(B, H, num_splits)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    if workspace.dtype != torch.uint8 or not workspace.is_cuda or not workspace.is_contiguous():
+        raise TypeError("workspace must be a contiguous uint8 GPU tensor")
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device)
+    rc = mla_decode_raw(q.data_ptr(), q_pe.data_ptr(), kv.data_ptr(), k_pe.data_ptr(),
+                        out.data_ptr(), lse.data_ptr(), B, H, Hkv, Skv, Dl, Dr, scale,
+                        num_splits, workspace.data_ptr(), workspace.numel(), stream.cuda_stream)
+    if rc != TA_OK:
+        raise TileAttnError(rc, ta_status_string(rc))
+    return out, lse

@@ -174,3 +174,51 @@ def test_split_heuristic_properties(shape):
         assert (n - 1) * wg < 512                 # no more splits than the target needs
     if n == 1 and wg < 512:
         assert n_kv // 32 <= 1                    # only when the keys are too short to split
+
+
+# mla_decode: argument errors before any HIP call (fake pointers)
+MQ, MQP, MKV, MKP, MO, ML, MWS = (0x10000000, 0x18000000, 0x20000000, 0x30000000, 0x40000000,
+                                  0x50000000, 0x60000000)
+MLA_OK = dict(Q=MQ, Qpe=MQP, KV=MKV, Kpe=MKP, O=MO, LSE=ML, B=2, H=128, Hkv=1, Skv=256, Dl=512,
+              Dr=64, scale=0.04, splits=2, ws=MWS, ws_bytes=1 << 24, stream=None)
+BAD_MLA = [
+    (dict(Q=0), 1), (dict(Qpe=0), 1), (dict(KV=0), 1), (dict(Kpe=0), 1), (dict(O=0), 1),
+    (dict(LSE=0), 1),
+    (dict(B=0), 2), (dict(H=0), 2), (dict(Hkv=0), 2), (dict(Skv=0), 2), (dict(H=128, Hkv=3), 2),
+    (dict(splits=0), 2), (dict(splits=129), 2),
+    (dict(Dl=256), 3), (dict(Dr=32), 3),
+    (dict(Q=MQ + 8), 4), (dict(KV=MKV + 2), 4), (dict(O=MO + 4), 4), (dict(ws=MWS + 8), 4),
+    (dict(scale=float("nan")), 5), (dict(scale=-1.0), 5),
+    (dict(O=MKV + 64), 6), (dict(LSE=MQ + 16), 6), (dict(LSE=MO + 1024), 6),
+    (dict(ws=MKP - 64), 6), (dict(ws=ML - 16), 6),
+    (dict(ws=0), 8), (dict(ws_bytes=2 * 2 * 128 * 513 * 4 - 1), 8),
+]
+
+
+@no_gpu
+@pytest.mark.parametrize("change,status", BAD_MLA, ids=[str(c) for c, _ in BAD_MLA])
+def test_mla_validation_before_any_hip_call(change, status):
+    a = dict(MLA_OK, **change)
+    rc = ta.mla_decode_raw(a["Q"], a["Qpe"], a["KV"], a["Kpe"], a["O"], a["LSE"], a["B"], a["H"],
+                           a["Hkv"], a["Skv"], a["Dl"], a["Dr"], a["scale"], a["splits"], a["ws"],
+                           a["ws_bytes"], a["stream"])
+    assert rc == status, f"{change}: got {ta.STATUS.get(rc, rc)}, want {ta.STATUS[status]}"
+
+
+def test_mla_workspace_and_heuristic():
+    assert ta.mla_workspace_bytes(64, 128, 4) == 4 * 64 * 128 * 513 * 4
+    assert ta.mla_workspace_bytes(64, 128, 1) == 0
+    with pytest.raises(ta.TileAttnError):
+        ta.mla_workspace_bytes(0, 128, 2)
+    for B, H, Hkv, Skv in [(64, 128, 1, 8192), (128, 128, 1, 4096), (1, 128, 1, 64),
+                           (2, 128, 1, 200), (8, 64, 2, 2048), (512, 128, 1, 4096)]:
+        n = ta.mla_split_heuristic(B, H, Hkv, Skv)
+        wg = B * Hkv * -(-(H // Hkv) // 64)
+        tiles = -(-Skv // 32)
+        assert 1 <= n <= 128
+        if wg >= 256:
+            assert n == 1
+        elif n > 1:
+            assert n <= tiles // 8 and (n - 1) * wg < 256
+        else:
+            assert tiles // 8 <= 1
