@@ -10,6 +10,9 @@ bounded sample of the same workload as a reported baseline.
                   [--splits 1|N|auto] [--no-cpu-baseline]
   python bench.py --copy-probe      # plain device copy of known size, for
                                     # scaling rocprofv3 FETCH_SIZE/WRITE_SIZE
+  python bench.py --workload mla_b64_s8k [--splits auto|N]
+                                    # one multi-head latent attention decode step
+                                    # (mla_decode) instead of attn_fwd
   python bench.py --sustain 8 [--gemm-reference]
                                     # run the step back to back for 8 s while
                                     # sampling board power and XCD clocks
@@ -173,12 +176,104 @@ def copy_probe(torch, mib: int = 1024, reps: int = 5):
                       "reps": reps}), flush=True)
 
 
+MLA_METRIC = "MLA decode TFLOP/s and % of MI355X bf16 MFMA peak, 1 GPU"
+
+
+def mla_cpu_baseline(w, q, q_pe, kv, k_pe, budget_s: float = 15.0):
+    """fp64 oracle throughput on whole batch elements of an MLA workload (all
+    heads each), as many as fit in about ``budget_s`` seconds."""
+    import oracle
+
+    threads = oracle.default_threads()
+    lib = oracle.load()
+
+    def heads(b):
+        return [(b, h) for h in range(w.H)]
+
+    t0 = time.perf_counter()
+    oracle.mla_rows(q, q_pe, kv, k_pe, w.scale, heads(0), nthreads=threads, lib=lib)
+    t1 = time.perf_counter() - t0
+    n_b = int(max(1, min(w.B - 1, budget_s / max(t1, 1e-6) - 1)))
+    rows = [r for b in range(1, 1 + n_b) for r in heads(b)]
+    t0 = time.perf_counter()
+    oracle.mla_rows(q, q_pe, kv, k_pe, w.scale, rows, nthreads=threads, lib=lib)
+    dt = time.perf_counter() - t0
+    flops = w.flops() / w.B * n_b
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n_b} of {w.B} batch elements of {w.name} (all {w.H} heads each), "
+                      f"fp64 C oracle, {dt:.1f} s wall"}
+
+
+def bench_mla(args, torch, tileattn):
+    """One MLA decode step per launch (plus the split merge when split)."""
+    import oracle
+
+    w = gen.MLA_WORKLOADS[args.workload]
+    q, q_pe, kv, k_pe = gen.make_mla_inputs(w, seed=args.seed)
+    dq, dqp, dkv, dkp = (to_device(x, torch) for x in (q, q_pe, kv, k_pe))
+    o = torch.empty((w.B, w.H, w.Dl), dtype=torch.float32, device="cuda")
+    lse = torch.empty((w.B, w.H), dtype=torch.float32, device="cuda")
+    n_split = (tileattn.mla_split_heuristic(w.B, w.H, w.Hkv, w.Skv) if args.splits == "auto"
+               else int(args.splits))
+    ws = torch.empty(max(16, tileattn.mla_workspace_bytes(w.B, w.H, n_split)), dtype=torch.uint8,
+                     device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        tileattn.mla_decode(dq, dqp, dkv, dkp, scale=w.scale, num_splits=n_split, out=o, lse=lse,
+                            workspace=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    rows = [(0, 0), (w.B - 1, w.H - 1), (w.B // 2, w.H // 2)]
+    ro, rl = oracle.mla_rows(q, q_pe, kv, k_pe, w.scale, rows)
+    idx = tuple(torch.tensor(c) for c in zip(*rows))
+    err_o = float(np.abs(o[idx].cpu().numpy() - ro).max())
+    err_l = float(np.abs(lse[idx].cpu().numpy() - rl).max())
+    if not (err_o <= 2e-2 and err_l <= 1e-3):
+        raise SystemExit(f"bench: result check failed (max|dO|={err_o}, max|dLSE|={err_l})")
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = start.elapsed_time(end) / args.steps
+    tflops = w.flops() / (ms * 1e-3) / 1e12
+    gbs = w.bytes() / (ms * 1e-3) / 1e9
+    result = {
+        "metric": MLA_METRIC, "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "splits": n_split, "data": "synthetic",
+        "config": {"workload": w.name, "shape": w.describe(), "B": w.B, "H": w.H, "Hkv": w.Hkv,
+                   "Skv": w.Skv, "Dl": w.Dl, "Dr": w.Dr, "seed": args.seed,
+                   "flops_per_step": w.flops(), "bytes_per_step": w.bytes()},
+        "pct_of_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None, "hbm_gbs_algorithmic": round(gbs, 1),
+                     "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)},
+        "wall_s_timed": round(wall, 4),
+        "check": {"max_abs_dO": err_o, "max_abs_dLSE": err_l, "rows": len(rows)},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = mla_cpu_baseline(w, q, q_pe, kv, k_pe)
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(gen.WORKLOADS))
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
+                    choices=sorted(gen.WORKLOADS) + sorted(gen.MLA_WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--out", choices=("f32", "bf16"), default="f32",
                     help="output dtype of O: attn_fwd (f32) or attn_fwd_bf16out (bf16)")
@@ -207,6 +302,9 @@ def main():
 
     if args.copy_probe:
         copy_probe(torch)
+        return
+    if args.workload in gen.MLA_WORKLOADS:
+        bench_mla(args, torch, tileattn)
         return
 
     w = gen.WORKLOADS[args.workload]

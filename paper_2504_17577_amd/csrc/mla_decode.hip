@@ -112,7 +112,52 @@ __device__ __forceinline__ float sum_halves(float x)
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-__device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+// Tile DMA is issued as inline assembly (buffer_load_dwordx4 ... lds), so
+// the compiler does not track it: it then never drains the tile loads in
+// flight before an LDS read (it cannot tell which buffer a DMA writes), and
+// the kernel waits for them itself with these vmcnt waits.  The kernel's
+// only other vector-memory operations are the query loads before the first
+// DMA and the output stores after the last wait.
+constexpr int DMA_PER_TILE = LAT_PER_THREAD + ROT_PER_THREAD;   // per thread
+__device__ __forceinline__ void wait_dma_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+__device__ __forceinline__ void wait_dma_but_one_tile()   // vmcnt(DMA_PER_TILE)
+{
+    static_assert(DMA_PER_TILE == 9, "vmcnt encoding below");
+    __builtin_amdgcn_s_waitcnt(0x0F79);
+}
+
+typedef uint32_t u32x4s __attribute__((ext_vector_type(4)));
+
+// A raw buffer resource (stride 0, 32-bit format, range-checked) in scalar
+// registers.
+__device__ __forceinline__ u32x4s buffer_rsrc(const void *base, uint32_t bytes)
+{
+    const uint64_t a = (uint64_t)(uintptr_t)base;
+    return u32x4s{(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a),
+                  (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32) & 0xFFFFu),
+                  (uint32_t)__builtin_amdgcn_readfirstlane(bytes), (uint32_t)BUF_RSRC_WORD3};
+}
+
+// One 16-byte-per-lane DMA: lane l's 16 bytes at byte `voff` of the buffer
+// land at LDS address `lds` + 16 l (`lds` wave-uniform).
+// M0 (which the compiler reserves) is saved and restored around the load.
+__device__ __forceinline__ void dma16(uint32_t lds, uint32_t voff, u32x4s rsrc)
+{
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\t"
+                 "s_mov_b32 m0, %1\n\t"
+                 "s_nop 0\n\t"
+                 "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
+                 "s_mov_b32 m0, %0"
+                 : "=&s"(saved)
+                 : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(rsrc)
+                 : "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void *p)
+{
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
 
 // LDS exchange between the two waves of a pair: each wave's partial scores
 // (its half of the 576-wide dot products) in the accumulator layout, and at
@@ -156,36 +201,31 @@ struct Mla {
     // are masked), so no lane addresses outside the cache.
     __device__ __forceinline__ void dma_tile(int j, unsigned char *lat, unsigned char *rot) const
     {
-#if __HIP_DEVICE_COMPILE__   // buffer-resource builtins exist in the device pass only
         const int valid = min(BN, a.Skv - j * BN);
         const size_t row0 = (size_t)j * BN * a.Hkv;
         const uint32_t lat_pitch = (uint32_t)a.Hkv * DL * 2, rot_pitch = (uint32_t)a.Hkv * DR * 2;
-        const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
-            (void *)(kv_b + row0 * DL), 0, (int)((valid - 1) * lat_pitch + DL * 2), BUF_RSRC_WORD3);
-        const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
-            (void *)(kpe_b + row0 * DR), 0, (int)((valid - 1) * rot_pitch + DR * 2), BUF_RSRC_WORD3);
+        const u32x4s rl = buffer_rsrc(kv_b + row0 * DL, (valid - 1) * lat_pitch + DL * 2);
+        const u32x4s rr = buffer_rsrc(kpe_b + row0 * DR, (valid - 1) * rot_pitch + DR * 2);
         const int wave_u = __builtin_amdgcn_readfirstlane(wave);
         const int last = valid - 1;
+        const uint32_t lat_base = lds_addr(lat), rot_base = lds_addr(rot);
 #pragma unroll
         for (int i = 0; i < LAT_PER_THREAD; ++i) {
             // row 4i + w, or the last valid row past it; lat_off[i & 3] holds
             // row 4(i & 3) + w.  (The difference can be negative: it is added
-            // to the vector offset modulo 2^32, never passed as soffset.)
+            // to the vector offset modulo 2^32.)
             const int row = 4 * i + wave_u;
             const int src = row > last ? last : row;
-            const uint32_t o = lat_off[i & 3] + (uint32_t)((src - 4 * (i & 3) - wave_u) * (int)lat_pitch);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rl, (lds_void *)(lat + (i * NT + wave_u * 64) * 16), 16, o, 0, 0, 0);
+            const uint32_t o =
+                lat_off[i & 3] + (uint32_t)((src - 4 * (i & 3) - wave_u) * (int)lat_pitch);
+            dma16(lat_base + (i * NT + wave_u * 64) * 16, o, rl);
         }
         {
             // row 8w + l/8 is lane-dependent: clamp per lane
             const int row = 8 * wave_u + lane / 8;
             const int shift = row > last ? row - last : 0;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rr, (lds_void *)(rot + wave_u * 64 * 16), 16,
-                                                     rot_off - (uint32_t)shift * rot_pitch, 0, 0,
-                                                     0);
+            dma16(rot_base + wave_u * 64 * 16, rot_off - (uint32_t)shift * rot_pitch, rr);
         }
-#endif
     }
 
     // Partial S^T[position][head] over this wave's 18 k-steps (288 of the
@@ -233,14 +273,15 @@ struct Mla {
                                          const unsigned char *rot, unsigned char *lat_n,
                                          unsigned char *rot_n, Xchg &x)
     {
-        if (j + 1 < j_hi)
-            dma_tile(j + 1, lat_n, rot_n);
         f32x16 s;
         scores<KH>(lat, rot, s);
 #pragma unroll
         for (int r = 0; r < 16; ++r)
             x.s[wave][r][lane] = s[r];
         __syncthreads();
+        // every wave is past tile j-1 now: its buffers take tile j+2
+        if (j + 2 < j_hi)
+            dma_tile(j + 2, lat_n, rot_n);
         // (k-half 0) + (k-half 1) in the same order on both waves, so that
         // the pair computes bitwise the same scores
 #pragma unroll
@@ -322,7 +363,11 @@ struct Mla {
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        wait_dma();
+        // tile j+1 must have landed (tile j+2's loads may stay in flight)
+        if (j + 2 < j_hi)
+            wait_dma_but_one_tile();
+        else
+            wait_dma_all();
         __syncthreads();
     }
 };
@@ -344,26 +389,35 @@ __device__ __forceinline__ void decode_wg(const MArgs &a, int bid, int &b, int &
     b = l / a.Hkv;
 }
 
-// The tile loop of one wave, KH = its k-half (wave-uniform).
+// The tile loop of one wave, KH = its k-half (wave-uniform).  Three
+// buffers in a ring: tile j lives in buffer (j - j_lo) % 3; the ring is
+// unrolled by three so that every buffer reference is static.
 template <int KH>
 __device__ __forceinline__ void run_tiles(Mla &k, int j_lo, int j_hi, int j_full,
-                                          unsigned char *lat0, unsigned char *rot0,
-                                          unsigned char *lat1, unsigned char *rot1, Xchg &xchg)
+                                          unsigned char *const (&lat)[3],
+                                          unsigned char *const (&rot)[3], Xchg &xchg)
 {
     int j = j_lo;
-    for (; j + 1 < j_full; j += 2) {
-        k.template step<false, KH>(j, j_hi, lat0, rot0, lat1, rot1, xchg);
-        k.template step<false, KH>(j + 1, j_hi, lat1, rot1, lat0, rot0, xchg);
+    for (; j + 2 < j_full; j += 3) {
+        k.template step<false, KH>(j, j_hi, lat[0], rot[0], lat[2], rot[2], xchg);
+        k.template step<false, KH>(j + 1, j_hi, lat[1], rot[1], lat[0], rot[0], xchg);
+        k.template step<false, KH>(j + 2, j_hi, lat[2], rot[2], lat[1], rot[1], xchg);
     }
+    // at most two full tiles and a ragged one remain: buffers continue at
+    // (j - j_lo) % 3 == 0
     if (j < j_full) {
-        k.template step<false, KH>(j, j_hi, lat0, rot0, lat1, rot1, xchg);
+        k.template step<false, KH>(j, j_hi, lat[0], rot[0], lat[2], rot[2], xchg);
         ++j;
-    }
-    if (j < j_hi) {   // the ragged last tile; its buffer parity follows j - j_lo
-        if ((j - j_lo) & 1)
-            k.template step<true, KH>(j, j_hi, lat1, rot1, lat0, rot0, xchg);
-        else
-            k.template step<true, KH>(j, j_hi, lat0, rot0, lat1, rot1, xchg);
+        if (j < j_full) {
+            k.template step<false, KH>(j, j_hi, lat[1], rot[1], lat[0], rot[0], xchg);
+            ++j;
+            if (j < j_hi)
+                k.template step<true, KH>(j, j_hi, lat[2], rot[2], lat[1], rot[1], xchg);
+        } else if (j < j_hi) {
+            k.template step<true, KH>(j, j_hi, lat[1], rot[1], lat[0], rot[0], xchg);
+        }
+    } else if (j < j_hi) {
+        k.template step<true, KH>(j, j_hi, lat[0], rot[0], lat[2], rot[2], xchg);
     }
 }
 
@@ -371,8 +425,10 @@ __global__ __launch_bounds__(NT, 1) void mla_decode_kernel(MArgs args)
 {
     __shared__ __attribute__((aligned(16))) unsigned char lat0[LAT_BYTES];
     __shared__ __attribute__((aligned(16))) unsigned char lat1[LAT_BYTES];
+    __shared__ __attribute__((aligned(16))) unsigned char lat2[LAT_BYTES];
     __shared__ __attribute__((aligned(16))) unsigned char rot0[ROT_BYTES];
     __shared__ __attribute__((aligned(16))) unsigned char rot1[ROT_BYTES];
+    __shared__ __attribute__((aligned(16))) unsigned char rot2[ROT_BYTES];
     __shared__ Xchg xchg;
 
     Mla k(args);
@@ -424,16 +480,24 @@ __global__ __launch_bounds__(NT, 1) void mla_decode_kernel(MArgs args)
     k.m_run = -INFINITY;
     k.l_run = 0.f;
 
+    // prologue: tiles j_lo and j_lo+1 in flight, wait for the first
     k.dma_tile(j_lo, lat0, rot0);
-    wait_dma();
+    if (j_lo + 1 < j_hi) {
+        k.dma_tile(j_lo + 1, lat1, rot1);
+        wait_dma_but_one_tile();
+    } else {
+        wait_dma_all();
+    }
     __syncthreads();
 
     // every tile but a ragged last one is fully valid
     const int j_full = min(j_hi, a.Skv / BN);
+    unsigned char *const lat[3] = {lat0, lat1, lat2};
+    unsigned char *const rot[3] = {rot0, rot1, rot2};
     if (k.k_half)
-        run_tiles<1>(k, j_lo, j_hi, j_full, lat0, rot0, lat1, rot1, xchg);
+        run_tiles<1>(k, j_lo, j_hi, j_full, lat, rot, xchg);
     else
-        run_tiles<0>(k, j_lo, j_hi, j_full, lat0, rot0, lat1, rot1, xchg);
+        run_tiles<0>(k, j_lo, j_hi, j_full, lat, rot, xchg);
 
     // epilogue: normalise and store this wave's 256 dims of the split's
     // result for the lane's head (both waves of the pair hold the same sums)
