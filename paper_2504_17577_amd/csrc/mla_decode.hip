@@ -119,11 +119,17 @@ __device__ __forceinline__ float sum_halves(float x)
 // only other vector-memory operations are the query loads before the first
 // DMA and the output stores after the last wait.
 constexpr int DMA_PER_TILE = LAT_PER_THREAD + ROT_PER_THREAD;   // per thread
-__device__ __forceinline__ void wait_dma_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
-__device__ __forceinline__ void wait_dma_but_one_tile()   // vmcnt(DMA_PER_TILE)
+static_assert(DMA_PER_TILE == 9, "vmcnt encodings below");
+// s_waitcnt vmcnt(n) (low 4 bits of n in [3:0], high 2 bits in [15:14]),
+// expcnt and lgkmcnt left at their maxima
+__device__ __forceinline__ void wait_dma_tiles_left(int tiles)   // tiles: 0, 1 or 2, uniform
 {
-    static_assert(DMA_PER_TILE == 9, "vmcnt encoding below");
-    __builtin_amdgcn_s_waitcnt(0x0F79);
+    if (tiles >= 2)
+        __builtin_amdgcn_s_waitcnt(0x4F72);   // vmcnt(18)
+    else if (tiles == 1)
+        __builtin_amdgcn_s_waitcnt(0x0F79);   // vmcnt(9)
+    else
+        __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
 }
 
 typedef uint32_t u32x4s __attribute__((ext_vector_type(4)));
@@ -163,7 +169,7 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p)
 // (its half of the 576-wide dot products) in the accumulator layout, and at
 // the end nothing else (both waves then hold identical softmax state)
 struct Xchg {
-    float s[4][16][64];
+    float4 s[4][4][64];   // [wave][r / 4][lane]: 16-byte accesses, lanes contiguous
 };
 
 struct Mla {
@@ -263,77 +269,11 @@ struct Mla {
         s = s0 + s1;
     }
 
-    // One cache tile: DMA of the next tile, partial scores, exchange with
-    // the partner wave (both then hold the same full scores), online
-    // softmax, O^T += V^T P^T over the tile's 32 positions for this wave's
-    // dims.  KH = k_half, a template argument so that the query's k-steps
-    // are indexed statically.
-    template <bool MASKED, int KH>
-    __device__ __forceinline__ void step(int j, int j_hi, const unsigned char *lat,
-                                         const unsigned char *rot, unsigned char *lat_n,
-                                         unsigned char *rot_n, Xchg &x)
+    // O^T += V^T P^T for one tile: the weights pk (B-operand layout) of its
+    // 32 positions and the transpose reads of its latent rows for this
+    // wave's 256 output dims
+    __device__ __forceinline__ void pv(const uint32_t (&pk)[8], const unsigned char *lat)
     {
-        f32x16 s;
-        scores<KH>(lat, rot, s);
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-            x.s[wave][r][lane] = s[r];
-        __syncthreads();
-        // every wave is past tile j-1 now: its buffers take tile j+2
-        if (j + 2 < j_hi)
-            dma_tile(j + 2, lat_n, rot_n);
-        // (k-half 0) + (k-half 1) in the same order on both waves, so that
-        // the pair computes bitwise the same scores
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const float o = x.s[wave ^ 1][r][lane];
-            s[r] = KH == 0 ? s[r] + o : o + s[r];
-        }
-
-        // lane holds positions j*BN + 8(r/4) + 4half + r%4 of head col
-        float mx = -INFINITY;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            if (MASKED) {
-                const int pos = j * BN + 8 * (r >> 2) + 4 * half + (r & 3);
-                s[r] = pos < a.Skv ? s[r] : -INFINITY;
-            }
-            mx = fmaxf(mx, s[r]);
-        }
-        mx = max_halves(mx);
-        const float m_tile = mx * a.c;   // every tile holds a valid position
-        if (__builtin_amdgcn_ballot_w64(m_tile > m_run + RESCALE_SLACK)) {
-            const float m_new = fmaxf(m_run, m_tile);
-            const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-            m_run = m_new;
-            l_run *= alpha;
-            // block by block through vector registers: the accumulator
-            // stays in the matrix-core registers everywhere else
-#pragma unroll
-            for (int db = 0; db < DBV; ++db) {
-                f32x16 t = acc_o[db];
-                asm volatile("" : "+v"(t));
-                t *= alpha;
-                asm volatile("" : "+v"(t));
-                acc_o[db] = t;
-                asm volatile("" : "+a"(acc_o[db]));
-            }
-        }
-        float rowsum = 0.f;
-        uint32_t pk[8];
-#pragma unroll
-        for (int r = 0; r < 16; r += 2) {
-            float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], a.c, -m_run));
-            float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r + 1], a.c, -m_run));
-            if (MASKED) {
-                p0 = s[r] == -INFINITY ? 0.f : p0;
-                p1 = s[r + 1] == -INFINITY ? 0.f : p1;
-            }
-            rowsum += p0 + p1;
-            pk[r >> 1] = pack_bf16(p0, p1);
-        }
-        l_run += rowsum;
-
         // MFMA k-slot t of half h stands for position 16ks + 4h + t (t < 4)
         // or 16ks + 8 + 4h + t-4, matching where the accumulator left P
         const int gq = lane >> 4, sl = lane & 15;
@@ -363,11 +303,90 @@ struct Mla {
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        // tile j+1 must have landed (tile j+2's loads may stay in flight)
-        if (j + 2 < j_hi)
-            wait_dma_but_one_tile();
-        else
-            wait_dma_all();
+    }
+
+    // One cache tile j, software-pipelined one tile deep: the partial
+    // scores of tile j, then the P V of tile j-1 (its weights pk from the
+    // previous step, its rows still in the previous buffer) while the
+    // partial scores travel to the partner wave; after the barrier, tile
+    // j+3 goes into that previous buffer, and the softmax of tile j leaves
+    // its weights in pk for the next step.  KH = k_half, a template argument
+    // so that the query's k-steps are indexed statically.
+    template <bool MASKED, int KH, bool PREV>
+    __device__ __forceinline__ void step(int j, int j_hi, const unsigned char *lat,
+                                         const unsigned char *rot, unsigned char *lat_p,
+                                         unsigned char *rot_p, uint32_t (&pk)[8], Xchg &x)
+    {
+        f32x16 s;
+        scores<KH>(lat, rot, s);
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4)
+            x.s[wave][r4][lane] = float4{s[4 * r4], s[4 * r4 + 1], s[4 * r4 + 2], s[4 * r4 + 3]};
+        if (PREV)
+            pv(pk, lat_p);
+        __syncthreads();
+        // every wave is past tile j-1 now: its buffers take tile j+3
+        if (j + 3 < j_hi)
+            dma_tile(j + 3, lat_p, rot_p);
+        // (k-half 0) + (k-half 1) in the same order on both waves, so that
+        // the pair computes bitwise the same scores
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+            const float4 o = x.s[wave ^ 1][r4][lane];
+            const float ov[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int r = 4 * r4 + e;
+                s[r] = KH == 0 ? s[r] + ov[e] : ov[e] + s[r];
+            }
+        }
+
+        // lane holds positions j*BN + 8(r/4) + 4half + r%4 of head col
+        float mx = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            if (MASKED) {
+                const int pos = j * BN + 8 * (r >> 2) + 4 * half + (r & 3);
+                s[r] = pos < a.Skv ? s[r] : -INFINITY;
+            }
+            mx = fmaxf(mx, s[r]);
+        }
+        mx = max_halves(mx);
+        const float m_tile = mx * a.c;   // every tile holds a valid position
+        if (__builtin_amdgcn_ballot_w64(m_tile > m_run + RESCALE_SLACK)) {
+            // acc already holds tile j-1, weighted with the old maximum
+            const float m_new = fmaxf(m_run, m_tile);
+            const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+            m_run = m_new;
+            l_run *= alpha;
+            // block by block through vector registers: the accumulator
+            // stays in the matrix-core registers everywhere else
+#pragma unroll
+            for (int db = 0; db < DBV; ++db) {
+                f32x16 t = acc_o[db];
+                asm volatile("" : "+v"(t));
+                t *= alpha;
+                asm volatile("" : "+v"(t));
+                acc_o[db] = t;
+                asm volatile("" : "+a"(acc_o[db]));
+            }
+        }
+        float rowsum = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) {
+            float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], a.c, -m_run));
+            float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r + 1], a.c, -m_run));
+            if (MASKED) {
+                p0 = s[r] == -INFINITY ? 0.f : p0;
+                p1 = s[r + 1] == -INFINITY ? 0.f : p1;
+            }
+            rowsum += p0 + p1;
+            pk[r >> 1] = pack_bf16(p0, p1);
+        }
+        l_run += rowsum;
+
+        // tile j+1 must have landed (tiles j+2 and j+3 may stay in flight)
+        wait_dma_tiles_left(min(2, max(0, j_hi - 1 - (j + 1))));
         __syncthreads();
     }
 };
@@ -389,35 +408,66 @@ __device__ __forceinline__ void decode_wg(const MArgs &a, int bid, int &b, int &
     b = l / a.Hkv;
 }
 
-// The tile loop of one wave, KH = its k-half (wave-uniform).  Three
-// buffers in a ring: tile j lives in buffer (j - j_lo) % 3; the ring is
-// unrolled by three so that every buffer reference is static.
+// The tile loop of one wave, KH = its k-half (wave-uniform).  Four
+// buffers in a ring: tile j lives in buffer (j - j_lo) % 4; tile j+3 goes
+// into the buffer of tile j-1 once every wave has done that tile's P V.  The
+// ring is unrolled by four so that every buffer reference is static; the
+// last tile's P V follows the loop.
 template <int KH>
 __device__ __forceinline__ void run_tiles(Mla &k, int j_lo, int j_hi, int j_full,
-                                          unsigned char *const (&lat)[3],
-                                          unsigned char *const (&rot)[3], Xchg &xchg)
+                                          unsigned char *const (&lat)[4],
+                                          unsigned char *const (&rot)[4], Xchg &xchg)
 {
+    uint32_t pk[8];
     int j = j_lo;
-    for (; j + 2 < j_full; j += 3) {
-        k.template step<false, KH>(j, j_hi, lat[0], rot[0], lat[2], rot[2], xchg);
-        k.template step<false, KH>(j + 1, j_hi, lat[1], rot[1], lat[0], rot[0], xchg);
-        k.template step<false, KH>(j + 2, j_hi, lat[2], rot[2], lat[1], rot[1], xchg);
-    }
-    // at most two full tiles and a ragged one remain: buffers continue at
-    // (j - j_lo) % 3 == 0
-    if (j < j_full) {
-        k.template step<false, KH>(j, j_hi, lat[0], rot[0], lat[2], rot[2], xchg);
-        ++j;
-        if (j < j_full) {
-            k.template step<false, KH>(j, j_hi, lat[1], rot[1], lat[0], rot[0], xchg);
-            ++j;
-            if (j < j_hi)
-                k.template step<true, KH>(j, j_hi, lat[2], rot[2], lat[1], rot[1], xchg);
-        } else if (j < j_hi) {
-            k.template step<true, KH>(j, j_hi, lat[1], rot[1], lat[0], rot[0], xchg);
+    // first tile: nothing before it to multiply into the output
+    if (j < j_full)
+        k.template step<false, KH, false>(j, j_hi, lat[0], rot[0], lat[3], rot[3], pk, xchg);
+    else
+        k.template step<true, KH, false>(j, j_hi, lat[0], rot[0], lat[3], rot[3], pk, xchg);
+    ++j;
+    int u = 1;   // buffer of tile j
+    if (j + 2 < j_full) {
+        for (; j + 3 < j_full; j += 4) {
+            k.template step<false, KH, true>(j, j_hi, lat[1], rot[1], lat[0], rot[0], pk, xchg);
+            k.template step<false, KH, true>(j + 1, j_hi, lat[2], rot[2], lat[1], rot[1], pk, xchg);
+            k.template step<false, KH, true>(j + 2, j_hi, lat[3], rot[3], lat[2], rot[2], pk, xchg);
+            k.template step<false, KH, true>(j + 3, j_hi, lat[0], rot[0], lat[3], rot[3], pk, xchg);
         }
-    } else if (j < j_hi) {
-        k.template step<true, KH>(j, j_hi, lat[0], rot[0], lat[2], rot[2], xchg);
+    }
+    // at most three full tiles and a ragged one remain; tile j is in buffer
+    // (j - j_lo) % 4
+    u = (j - j_lo) & 3;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        if (j >= j_hi)
+            break;
+        // (buffers indexed at run time here: these remaining tiles are few)
+        switch (u) {
+#define TA_MLA_STEP(U)                                                                          \
+    case U:                                                                                     \
+        if (j < j_full)                                                                         \
+            k.template step<false, KH, true>(j, j_hi, lat[U], rot[U], lat[(U + 3) % 4],          \
+                                             rot[(U + 3) % 4], pk, xchg);                        \
+        else                                                                                    \
+            k.template step<true, KH, true>(j, j_hi, lat[U], rot[U], lat[(U + 3) % 4],           \
+                                            rot[(U + 3) % 4], pk, xchg);                         \
+        break;
+            TA_MLA_STEP(0)
+            TA_MLA_STEP(1)
+            TA_MLA_STEP(2)
+            TA_MLA_STEP(3)
+#undef TA_MLA_STEP
+        }
+        ++j;
+        u = (u + 1) & 3;
+    }
+    // the last tile's P V (its buffer is that of tile j_hi - 1)
+    switch ((j_hi - 1 - j_lo) & 3) {
+    case 0: k.pv(pk, lat[0]); break;
+    case 1: k.pv(pk, lat[1]); break;
+    case 2: k.pv(pk, lat[2]); break;
+    default: k.pv(pk, lat[3]); break;
     }
 }
 
@@ -426,9 +476,11 @@ __global__ __launch_bounds__(NT, 1) void mla_decode_kernel(MArgs args)
     __shared__ __attribute__((aligned(16))) unsigned char lat0[LAT_BYTES];
     __shared__ __attribute__((aligned(16))) unsigned char lat1[LAT_BYTES];
     __shared__ __attribute__((aligned(16))) unsigned char lat2[LAT_BYTES];
+    __shared__ __attribute__((aligned(16))) unsigned char lat3[LAT_BYTES];
     __shared__ __attribute__((aligned(16))) unsigned char rot0[ROT_BYTES];
     __shared__ __attribute__((aligned(16))) unsigned char rot1[ROT_BYTES];
     __shared__ __attribute__((aligned(16))) unsigned char rot2[ROT_BYTES];
+    __shared__ __attribute__((aligned(16))) unsigned char rot3[ROT_BYTES];
     __shared__ Xchg xchg;
 
     Mla k(args);
@@ -480,20 +532,19 @@ __global__ __launch_bounds__(NT, 1) void mla_decode_kernel(MArgs args)
     k.m_run = -INFINITY;
     k.l_run = 0.f;
 
-    // prologue: tiles j_lo and j_lo+1 in flight, wait for the first
+    // prologue: tiles j_lo .. j_lo+2 in flight, wait for the first
     k.dma_tile(j_lo, lat0, rot0);
-    if (j_lo + 1 < j_hi) {
+    if (j_lo + 1 < j_hi)
         k.dma_tile(j_lo + 1, lat1, rot1);
-        wait_dma_but_one_tile();
-    } else {
-        wait_dma_all();
-    }
+    if (j_lo + 2 < j_hi)
+        k.dma_tile(j_lo + 2, lat2, rot2);
+    wait_dma_tiles_left(min(2, j_hi - 1 - j_lo));
     __syncthreads();
 
     // every tile but a ragged last one is fully valid
     const int j_full = min(j_hi, a.Skv / BN);
-    unsigned char *const lat[3] = {lat0, lat1, lat2};
-    unsigned char *const rot[3] = {rot0, rot1, rot2};
+    unsigned char *const lat[4] = {lat0, lat1, lat2, lat3};
+    unsigned char *const rot[4] = {rot0, rot1, rot2, rot3};
     if (k.k_half)
         run_tiles<1>(k, j_lo, j_hi, j_full, lat, rot, xchg);
     else
