@@ -149,3 +149,35 @@ def mla_rows(q, q_pe, kv, k_pe, scale: float, rows, nthreads: int | None = None,
     idx = [(int(b), int(h), 0) for b, h in rows]
     o, lse = attn_rows(qf, kf, kf, False, scale, idx, nthreads=nthreads, lib=lib)
     return np.ascontiguousarray(o[:, :Dl]), lse
+
+
+# ---------------------------------------------------------------------------
+# Matrix multiplication (the paper's Matmul listing): C = A B for row-major
+# A [M, K] and B [K, N] given as bfloat16 bits.  The definition, in float64:
+# the inputs widen exactly and numpy's matmul forms the products and sums.
+# ``gemm_abs`` is sum_k |a_ik| |b_kj|, the scale the GPU tolerance is stated
+# against.
+
+def _widen(bits):
+    b = np.ascontiguousarray(bits)
+    if b.dtype != np.uint16 or b.ndim != 2:
+        raise TypeError("GEMM oracle inputs are 2-D bfloat16 bit arrays (numpy.uint16)")
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+
+
+def gemm(a, b, rows=None):
+    """C = A B in float64 (all rows, or only the rows listed in ``rows``)."""
+    A, B = _widen(a), _widen(b)
+    if A.shape[1] != B.shape[0]:
+        raise OracleError(f"inconsistent GEMM shapes a{A.shape} b{B.shape}")
+    if rows is not None:
+        A = A[np.asarray(rows, dtype=np.int64)]
+    return A @ B
+
+
+def gemm_abs(a, b, rows=None):
+    """sum_k |a_ik| |b_kj| in float64, for the same rows as ``gemm``."""
+    A, B = np.abs(_widen(a)), np.abs(_widen(b))
+    if rows is not None:
+        A = A[np.asarray(rows, dtype=np.int64)]
+    return A @ B

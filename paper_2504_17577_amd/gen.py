@@ -231,3 +231,56 @@ def make_mla_inputs(w: MlaWorkload, seed: int = 0):
 def random_mla_problem(B, H, Hkv, Skv, seed: int, Dl: int = 512, Dr: int = 64, wid: int = 101):
     """(q, q_pe, kv, k_pe) bfloat16 bits for an ad-hoc MLA shape."""
     return make_mla_inputs(MlaWorkload("adhoc", wid, B, H, Hkv, Skv, Dl, Dr), seed)
+
+
+# ---------------------------------------------------------------------------
+# Matrix multiplication C = A B (the paper's Matmul listing: A [M, K] and
+# B [K, N] row-major, tiles of C accumulated over K).  The shapes are the
+# paper's M0-M7 (appendix table "Matrix shapes in our benchmark"); A and B
+# i.i.d. N(0,1) in bf16.
+
+@dataclasses.dataclass(frozen=True)
+class GemmWorkload:
+    name: str
+    wid: int
+    M: int
+    N: int
+    K: int
+
+    def flops(self) -> int:
+        return 2 * self.M * self.N * self.K
+
+    def bytes(self, c_bytes: int = 2) -> int:
+        """A and B read once (bf16), C written once."""
+        return 2 * (self.M * self.K + self.K * self.N) + c_bytes * self.M * self.N
+
+    def describe(self) -> str:
+        return f"M={self.M} N={self.N} K={self.K}"
+
+
+GEMM_WORKLOADS = {
+    w.name: w
+    for w in (
+        GemmWorkload("gemm_tiny", 40, 256, 384, 192),
+        GemmWorkload("gemm_m0", 41, 4096, 1024, 8192),
+        GemmWorkload("gemm_m1", 42, 4096, 8192, 8192),
+        GemmWorkload("gemm_m2", 43, 4096, 28672, 8192),
+        GemmWorkload("gemm_m3", 44, 4096, 8192, 28672),
+        GemmWorkload("gemm_m4", 45, 8192, 1024, 8192),
+        GemmWorkload("gemm_m5", 46, 8192, 8192, 8192),
+        GemmWorkload("gemm_m6", 47, 8192, 28672, 8192),
+        GemmWorkload("gemm_m7", 48, 8192, 8192, 28672),
+    )
+}
+
+TENSOR_A, TENSOR_B = 5, 6
+
+
+def make_gemm_inputs(w: GemmWorkload, seed: int = 0):
+    """(a [M, K], b [K, N]) bfloat16 bit arrays for GEMM workload ``w``."""
+    return (normal_bf16((w.M, w.K), seed, w.wid, TENSOR_A),
+            normal_bf16((w.K, w.N), seed, w.wid, TENSOR_B))
+
+
+def random_gemm_problem(M: int, N: int, K: int, seed: int, wid: int = 102):
+    return make_gemm_inputs(GemmWorkload("adhoc", wid, M, N, K), seed)
