@@ -10,6 +10,9 @@ bounded sample of the same workload as a reported baseline.
                   [--splits 1|N|auto] [--no-cpu-baseline]
   python bench.py --copy-probe      # plain device copy of known size, for
                                     # scaling rocprofv3 FETCH_SIZE/WRITE_SIZE
+  python bench.py --workload gemm_m5 [--out f32|bf16]
+                                    # C = A B (gemm_bf16) at one of the paper's
+                                    # M0-M7 shapes, with hipBLASLt timed beside it
   python bench.py --workload mla_b64_s8k [--splits auto|N]
                                     # one multi-head latent attention decode step
                                     # (mla_decode) instead of attn_fwd
@@ -267,16 +270,98 @@ def bench_mla(args, torch, tileattn):
     print(json.dumps(result), flush=True)
 
 
+GEMM_METRIC = "GEMM TFLOP/s and % of MI355X bf16 MFMA peak, 1 GPU"
+
+
+def bench_gemm(args, torch, tileattn):
+    """C = A B at a GEMM workload; torch.matmul (hipBLASLt) on the same
+    operands is timed the same way as a reference."""
+    import oracle
+
+    w = gen.GEMM_WORKLOADS[args.workload]
+    a, b = gen.make_gemm_inputs(w, seed=args.seed)
+    da, db = to_device(a, torch), to_device(b, torch)
+    c_bf16 = args.out != "f32"
+    dt = torch.bfloat16 if c_bf16 else torch.float32
+    c = torch.empty((w.M, w.N), dtype=dt, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        tileattn.gemm_bf16(da, db, out=c, out_dtype=dt, stream=stream)
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        start.record(stream)
+        for _ in range(args.steps):
+            fn()
+        end.record(stream)
+        torch.cuda.synchronize()
+        return start.elapsed_time(end) / args.steps, time.perf_counter() - t0
+
+    ms, wall = timed(step)
+    rows = [0, w.M // 2, w.M - 1]
+    ref = oracle.gemm(a, b, rows=rows)
+    scale = oracle.gemm_abs(a, b, rows=rows)
+    got = c.float()[torch.tensor(rows)].cpu().numpy()
+    tol = 1e-5 * scale + (2.0 ** -8 * np.abs(ref) if c_bf16 else 0.0)
+    worst = float((np.abs(got - ref) / tol).max())
+    if not worst <= 1.0:
+        raise SystemExit(f"bench: result check failed (worst err/tol {worst})")
+    ref_out = torch.empty((w.M, w.N), dtype=torch.bfloat16, device="cuda")
+    ms_ref, _ = timed(lambda: torch.matmul(da, db, out=ref_out))
+    tflops = w.flops() / (ms * 1e-3) / 1e12
+    result = {
+        "metric": GEMM_METRIC, "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "out_dtype": "bf16" if c_bf16 else "f32", "data": "synthetic",
+        "config": {"workload": w.name, "shape": w.describe(), "M": w.M, "N": w.N, "K": w.K,
+                   "seed": args.seed, "flops_per_step": w.flops()},
+        "pct_of_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None,
+                     "hbm_gbs_algorithmic": round(w.bytes(2 if c_bf16 else 4) / (ms * 1e-3) / 1e9, 1)},
+        "vendor_reference": {"op": "torch.matmul bf16 -> bf16 (hipBLASLt)",
+                             "tflops": round(w.flops() / (ms_ref * 1e-3) / 1e12, 2),
+                             "ms_per_call": round(ms_ref, 5),
+                             "ratio": round(ms_ref / ms, 4)},
+        "wall_s_timed": round(wall, 4),
+        "check": {"worst_err_over_tol": worst, "rows": len(rows)},
+    }
+    if not args.no_cpu_baseline:
+        # fp64 oracle on a bounded number of rows (about 10 s)
+        t0 = time.perf_counter()
+        oracle.gemm(a, b, rows=[0])
+        t1 = max(time.perf_counter() - t0, 1e-6)
+        n = int(max(1, min(w.M, 10.0 / t1)))
+        t0 = time.perf_counter()
+        oracle.gemm(a, b, rows=list(range(n)))
+        dt_s = time.perf_counter() - t0
+        result["cpu_baseline"] = {
+            "value": 2.0 * n * w.N * w.K / dt_s / 1e12, "unit": "TFLOP/s",
+            "cores": len(os.sched_getaffinity(0)), "kind": "oracle",
+            "sample": f"{n} of {w.M} rows of {w.name}, float64 numpy matmul, {dt_s:.1f} s wall"}
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
-                    choices=sorted(gen.WORKLOADS) + sorted(gen.MLA_WORKLOADS))
+                    choices=sorted(gen.WORKLOADS) + sorted(gen.MLA_WORKLOADS)
+                    + sorted(gen.GEMM_WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--out", choices=("f32", "bf16"), default="f32",
-                    help="output dtype of O: attn_fwd (f32) or attn_fwd_bf16out (bf16)")
+    ap.add_argument("--out", choices=("f32", "bf16"), default=None,
+                    help="output dtype: attention O f32 (default, attn_fwd) or bf16 "
+                         "(attn_fwd_bf16out); GEMM C bf16 (default) or f32")
     ap.add_argument("--splits", default="1",
                     help="key splits per query tile: 1 (attn_fwd), N or auto "
                          "(attn_fwd_split with ta_split_heuristic; workspace allocated "
@@ -306,6 +391,11 @@ def main():
     if args.workload in gen.MLA_WORKLOADS:
         bench_mla(args, torch, tileattn)
         return
+    if args.workload in gen.GEMM_WORKLOADS:
+        bench_gemm(args, torch, tileattn)
+        return
+    if args.out is None:
+        args.out = "f32"
 
     w = gen.WORKLOADS[args.workload]
     q, k, v = gen.make_inputs(w, seed=args.seed)

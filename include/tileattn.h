@@ -173,6 +173,22 @@ ta_status mla_workspace_bytes(int B, int H, int num_splits, size_t *bytes);
 ta_status mla_split_heuristic(int B, int H, int Hkv, int Skv, int *num_splits);
 
 /*
+ * gemm_bf16 — C = A B: the kernel beneath the paper's Matmul listing
+ * (appendix "Matrix Multiplication (Matmul)"), bf16 inputs, fp32
+ * accumulation.
+ *
+ *   A  device, bf16 [M, K] row-major         read only
+ *   B  device, bf16 [K, N] row-major         read only
+ *   C  device, [M, N] row-major: fp32, or bf16 (rounded to nearest even) if
+ *      c_bf16 != 0                             written
+ *   M % 128 == 0, N % 128 == 0, K % 64 == 0 (else TA_ERR_UNSUPPORTED); every
+ *   pointer 16-byte aligned; C must not overlap A or B; stream as attn_fwd.
+ * Status codes as attn_fwd; validation before any HIP call.
+ */
+ta_status gemm_bf16(const void *A, const void *B, void *C, int c_bf16, int M, int N, int K,
+                    void *stream);
+
+/*
  * ta_schedule — host-side tile schedule of attn_fwd, for tests and tools.
  * For the query tile `q_tile` (rows q_tile*BM .. q_tile*BM+BM-1, BM from
  * ta_tile_shape) it reports how many key tiles of BN keys the kernel visits

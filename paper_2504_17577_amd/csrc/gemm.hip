@@ -1,0 +1,310 @@
+// bf16 matrix multiplication C = A B for gfx950 (MI355X): the kernel beneath
+// the paper's Matmul listing (appendix "Matrix Multiplication (Matmul)":
+// tiles of A [M, K] and B [K, N], row-major, copied to shared memory per
+// K-step and multiplied into a register tile of C).  The design is this
+// library's own for CDNA4:
+//
+//  * One workgroup of four wave64s computes a BM x BN tile of C (256 x 256,
+//    or 128 x 128 when the grid of large tiles would not fill the GPU); the
+//    waves form a 2 x 2 grid, each owning (BM/2) x (BN/2) as 32 x 32 blocks
+//    of v_mfma_f32_32x32x16_bf16 accumulators (fp32).
+//  * K advances in steps of 64.  The A tile [BM][64] and the B tile [64][BN]
+//    go global -> LDS by DMA (buffer_load_dwordx4 ... lds, issued as inline
+//    assembly and waited for explicitly), double-buffered: the DMA of step
+//    k+1 runs under the MFMAs of step k.
+//  * A operands (32 rows x 8 consecutive k per lane) are ds_read_b128 from
+//    the A tile, 16-byte chunk c of row r stored at c ^ ((r >> 1) & 7).  B
+//    operands (8 consecutive k of one column per lane) come from the
+//    row-major B tile through the transpose read ds_read_b64_tr_b16, chunk c
+//    of row r stored at c ^ 4 (r & 3).  Both swizzles make the operand reads
+//    bank-conflict free.
+//  * The grid maps workgroups so that each XCD gets a contiguous range of
+//    tiles, row-major over the tiles of C, so neighbouring tiles that share
+//    rows of A run on one XCD's L2.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tileattn.h"
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+constexpr int BK = 64;       // K per stage
+constexpr int NT = 256;      // threads per workgroup (4 waves)
+constexpr int NXCD = 8;
+[[maybe_unused]] constexpr int BUF_RSRC_WORD3 = 0x00020000;
+
+struct GArgs {
+    const uint16_t *A, *B;
+    void *C;
+    int M, N, K;
+    int tiles_n;     // N / BN
+    int n_wg;
+};
+
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c)
+{
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
+}
+
+// The tile DMA is inline assembly, untracked by the compiler (it would
+// otherwise drain the loads in flight before every LDS read, unable to tell
+// which buffer they write); the loop waits for it with vmcnt(0).
+__device__ __forceinline__ void wait_dma_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+typedef uint32_t u32x4s __attribute__((ext_vector_type(4)));
+
+// raw buffer resource (stride 0, 32-bit format, range-checked) in SGPRs
+__device__ __forceinline__ u32x4s buffer_rsrc(const void *base, uint32_t bytes)
+{
+    const uint64_t a = (uint64_t)(uintptr_t)base;
+    return u32x4s{(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a),
+                  (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32) & 0xFFFFu),
+                  (uint32_t)__builtin_amdgcn_readfirstlane(bytes), (uint32_t)BUF_RSRC_WORD3};
+}
+
+// lane l's 16 bytes at byte `voff` of the buffer land at LDS `lds` + 16 l
+// (`lds` wave-uniform); M0 is saved and restored around the load
+__device__ __forceinline__ void dma16(uint32_t lds, uint32_t voff, u32x4s rsrc)
+{
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\t"
+                 "s_mov_b32 m0, %1\n\t"
+                 "s_nop 0\n\t"
+                 "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
+                 "s_mov_b32 m0, %0"
+                 : "=&s"(saved)
+                 : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(rsrc)
+                 : "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void *p)
+{
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
+__device__ __forceinline__ int a_swz(int r) { return (r >> 1) & 7; }
+__device__ __forceinline__ int b_swz(int r) { return 4 * (r & 3); }
+
+template <int BM, int BN>
+struct Cfg {
+    static constexpr int WM = BM / 2, WN = BN / 2;        // wave tile
+    static constexpr int FM = WM / 32, FN = WN / 32;      // 32 x 32 blocks per wave
+    static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BK * BN * 2;
+    static constexpr int A_PER_THREAD = BM * (BK / 8) / NT;   // 16-byte slots
+    static constexpr int B_PER_THREAD = BK * (BN / 8) / NT;
+    static constexpr int BCH = BN / 8;                    // 16-byte chunks per B row
+};
+
+template <int BM, int BN, bool CBF16>
+__global__ __launch_bounds__(NT, BM == 256 ? 1 : 2) void gemm_kernel(GArgs args)
+{
+    using C = Cfg<BM, BN>;
+    __shared__ __attribute__((aligned(16))) unsigned char a0[C::A_BYTES];
+    __shared__ __attribute__((aligned(16))) unsigned char a1[C::A_BYTES];
+    __shared__ __attribute__((aligned(16))) unsigned char b0[C::B_BYTES];
+    __shared__ __attribute__((aligned(16))) unsigned char b1[C::B_BYTES];
+
+    const GArgs &a = args;
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6, lane = tid & 63;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const int col = lane & 31, half = lane >> 5;
+
+    // XCD-contiguous logical tile index, row-major over the tiles of C
+    const int per = a.n_wg / NXCD, rem = a.n_wg % NXCD;
+    const int xcd = blockIdx.x % NXCD, idx = blockIdx.x / NXCD;
+    const int t = xcd * per + (xcd < rem ? xcd : rem) + idx;
+    const int m0 = (t / a.tiles_n) * BM, n0 = (t % a.tiles_n) * BN;
+    const int wm = (wave >> 1) * C::WM, wn = (wave & 1) * C::WN;
+
+    // per-lane DMA source offsets within a stage's tiles.  A slot
+    // i*NT + 64w + l is row s / 8, stored chunk s % 8 (fetched from chunk
+    // (s % 8) ^ a_swz(row)); B slot s is row s / BCH, stored chunk s % BCH
+    // (fetched from chunk (s % BCH) ^ b_swz(row)).
+    uint32_t a_off[C::A_PER_THREAD], b_off[C::B_PER_THREAD];
+#pragma unroll
+    for (int i = 0; i < C::A_PER_THREAD; ++i) {
+        const int s = i * NT + wave_u * 64 + lane;
+        const int r = s / 8, sc = s % 8;
+        a_off[i] = (uint32_t)r * a.K * 2 + 16 * (sc ^ a_swz(r));
+    }
+#pragma unroll
+    for (int i = 0; i < C::B_PER_THREAD; ++i) {
+        const int s = i * NT + wave_u * 64 + lane;
+        const int r = s / C::BCH, sc = s % C::BCH;
+        b_off[i] = (uint32_t)r * a.N * 2 + 16 * (sc ^ b_swz(r));
+    }
+
+    auto dma = [&](int kt, unsigned char *as, unsigned char *bs) {
+        const int k0 = kt * BK;
+        const u32x4s ra = buffer_rsrc(a.A + (size_t)m0 * a.K + k0,
+                                      (uint32_t)((BM - 1) * a.K + BK) * 2);
+        const u32x4s rb = buffer_rsrc(a.B + (size_t)k0 * a.N + n0,
+                                      (uint32_t)((BK - 1) * a.N + BN) * 2);
+        const uint32_t la = lds_addr(as), lb = lds_addr(bs);
+#pragma unroll
+        for (int i = 0; i < C::A_PER_THREAD; ++i)
+            dma16(la + (i * NT + wave_u * 64) * 16, a_off[i], ra);
+#pragma unroll
+        for (int i = 0; i < C::B_PER_THREAD; ++i)
+            dma16(lb + (i * NT + wave_u * 64) * 16, b_off[i], rb);
+    };
+
+    f32x16 acc[C::FM][C::FN];
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[i][j][r] = 0.f;
+
+    // B operand transpose-read addressing (per 16-lane group g = lane / 16,
+    // s = lane % 16): rows 16ks + 8(g >> 1) + (s >> 2) and + 4, columns
+    // 16(g & 1) + 4(s & 3) of each 32-column block: the lane then holds 8
+    // consecutive k of one column, k-slot t <-> k = 16ks + 8 half + t
+    const int g = lane >> 4, sl = lane & 15;
+    const int b_row = 8 * (g >> 1) + (sl >> 2);
+    const int b_col = 16 * (g & 1) + 4 * (sl & 3);
+
+    auto compute = [&](const unsigned char *as, const unsigned char *bs) {
+#pragma unroll
+        for (int ks = 0; ks < BK / 16; ++ks) {
+            bf16x8 av[C::FM], bv[C::FN];
+#pragma unroll
+            for (int i = 0; i < C::FM; ++i) {
+                const int r = wm + 32 * i + col;
+                av[i] = *(const bf16x8 *)(as + r * (BK * 2) + 16 * ((2 * ks + half) ^ a_swz(r)));
+            }
+#pragma unroll
+            for (int j = 0; j < C::FN; ++j) {
+                const int n = wn + 32 * j + b_col;
+                const int r0 = 16 * ks + b_row, r1 = r0 + 4;
+                const unsigned char *p0 =
+                    bs + r0 * (BN * 2) + 16 * ((n >> 3) ^ b_swz(r0)) + 2 * (n & 7);
+                const unsigned char *p1 =
+                    bs + r1 * (BN * 2) + 16 * ((n >> 3) ^ b_swz(r1)) + 2 * (n & 7);
+                const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p0);
+                const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p1);
+                const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+                bv[j] = __builtin_bit_cast(bf16x8, u32x4{l2[0], l2[1], h2[0], h2[1]});
+            }
+#pragma unroll
+            for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+                for (int j = 0; j < C::FN; ++j)
+                    acc[i][j] = mfma32(av[i], bv[j], acc[i][j]);
+        }
+    };
+
+    const int n_kt = a.K / BK;
+    dma(0, a0, b0);
+    wait_dma_all();
+    __syncthreads();
+    int kt = 0;
+    for (; kt + 1 < n_kt; kt += 2) {
+        dma(kt + 1, a1, b1);
+        compute(a0, b0);
+        wait_dma_all();
+        __syncthreads();
+        if (kt + 2 < n_kt)
+            dma(kt + 2, a0, b0);
+        compute(a1, b1);
+        wait_dma_all();
+        __syncthreads();
+    }
+    if (kt < n_kt)
+        compute(a0, b0);
+
+    // epilogue: lane holds column wn + 32j + col, rows wm + 32i + 8(r/4) +
+    // 4half + r%4 of the tile
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j) {
+            const int n = n0 + wn + 32 * j + col;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int m = m0 + wm + 32 * i + 8 * (r >> 2) + 4 * half + (r & 3);
+                if (CBF16)
+                    ((uint16_t *)a.C)[(size_t)m * a.N + n] =
+                        (uint16_t)pack_bf16(acc[i][j][r], 0.f);
+                else
+                    ((float *)a.C)[(size_t)m * a.N + n] = acc[i][j][r];
+            }
+        }
+}
+
+bool misaligned(const void *p) { return ((uintptr_t)p & 15u) != 0; }
+
+bool overlaps(const void *p, size_t pn, const void *q, size_t qn)
+{
+    const uintptr_t x = (uintptr_t)p, y = (uintptr_t)q;
+    return x < y + qn && y < x + pn;
+}
+
+template <int BM, int BN>
+hipError_t launch(GArgs &a, bool c_bf16, hipStream_t s)
+{
+    a.tiles_n = a.N / BN;
+    a.n_wg = (a.M / BM) * a.tiles_n;
+    if (c_bf16)
+        hipLaunchKernelGGL((gemm_kernel<BM, BN, true>), dim3(a.n_wg), dim3(NT), 0, s, a);
+    else
+        hipLaunchKernelGGL((gemm_kernel<BM, BN, false>), dim3(a.n_wg), dim3(NT), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+extern "C" {
+
+ta_status gemm_bf16(const void *A, const void *B, void *C, int c_bf16, int M, int N, int K,
+                    void *stream)
+{
+    if (!A || !B || !C)
+        return TA_ERR_NULL_POINTER;
+    if (M < 1 || N < 1 || K < 1)
+        return TA_ERR_INVALID_SHAPE;
+    if (M % 128 || N % 128 || K % BK)
+        return TA_ERR_UNSUPPORTED;
+    // 32-bit offsets within a workgroup's tiles and buffer ranges
+    if ((int64_t)K * N * 2 >= (1ll << 31) || (int64_t)M * K >= (1ll << 40) ||
+        (int64_t)256 * K * 2 >= (1ll << 31))
+        return TA_ERR_INVALID_SHAPE;
+    if (misaligned(A) || misaligned(B) || misaligned(C))
+        return TA_ERR_MISALIGNED;
+    const size_t a_bytes = (size_t)M * K * 2, b_bytes = (size_t)K * N * 2;
+    const size_t c_bytes = (size_t)M * N * (c_bf16 ? 2 : 4);
+    if (overlaps(C, c_bytes, A, a_bytes) || overlaps(C, c_bytes, B, b_bytes))
+        return TA_ERR_ALIASING;
+    GArgs a;
+    a.A = (const uint16_t *)A;
+    a.B = (const uint16_t *)B;
+    a.C = C;
+    a.M = M;
+    a.N = N;
+    a.K = K;
+    hipStream_t s = (hipStream_t)stream;
+    // 256 x 256 tiles when they give at least one workgroup per CU
+    const bool big = M % 256 == 0 && N % 256 == 0 && (int64_t)(M / 256) * (N / 256) >= 256;
+    const hipError_t e = big ? launch<256, 256>(a, c_bf16 != 0, s)
+                             : launch<128, 128>(a, c_bf16 != 0, s);
+    return e == hipSuccess ? TA_OK : TA_ERR_LAUNCH;
+}
+
+}  // extern "C"

@@ -57,6 +57,8 @@ def lib():
     L.mla_workspace_bytes.argtypes = [i, i, i, ctypes.POINTER(ctypes.c_size_t)]
     L.mla_split_heuristic.restype = i
     L.mla_split_heuristic.argtypes = [i, i, i, i, ctypes.POINTER(i)]
+    L.gemm_bf16.restype = i
+    L.gemm_bf16.argtypes = [p, p, p, i, i, i, i, p]
     L.ta_schedule.restype = i
     L.ta_schedule.argtypes = [i, i, i, i, i, ctypes.POINTER(i), ctypes.POINTER(i)]
     L.ta_tile_shape.restype = i
@@ -278,3 +280,36 @@ def mla_decode(q, q_pe, kv, k_pe, scale: float | None = None, num_splits: int | 
     if rc != TA_OK:
         raise TileAttnError(rc, ta_status_string(rc))
     return out, lse
+
+
+def gemm_bf16_raw(A, B, C, c_bf16, M, N, K, stream) -> int:
+    """gemm_bf16 with integer pointers; returns the status code."""
+    return lib().gemm_bf16(A, B, C, int(bool(c_bf16)), M, N, K, stream)
+
+
+def gemm_bf16(a, b, out=None, out_dtype=None, stream=None):
+    """C = A B for contiguous bfloat16 GPU matrices a [M, K], b [K, N]; C is
+    float32 (default) or bfloat16 (``out_dtype=torch.bfloat16``)."""
+    import torch
+
+    for name, t in (("a", a), ("b", b)):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or t.dim() != 2 or not t.is_contiguous():
+            raise TypeError(f"{name} must be a contiguous 2-D bfloat16 GPU tensor")
+    M, K = a.shape
+    K2, N = b.shape
+    if K2 != K:
+        raise TileAttnError(2, f"inconsistent shapes a{tuple(a.shape)} b{tuple(b.shape)}")
+    dt = torch.float32 if out_dtype is None else out_dtype
+    if dt not in (torch.float32, torch.bfloat16):
+        raise TypeError("out_dtype must be torch.float32 or torch.bfloat16")
+    if out is None:
+        out = torch.empty((M, N), dtype=dt, device=a.device)
+    if out.dtype != dt or tuple(out.shape) != (M, N) or not out.is_contiguous():
+        raise TypeError(f"out must be a contiguous {dt} tensor of shape {(M, N)}")
+    if stream is None:
+        stream = torch.cuda.current_stream(a.device)
+    rc = gemm_bf16_raw(a.data_ptr(), b.data_ptr(), out.data_ptr(), dt == torch.bfloat16, M, N, K,
+                       stream.cuda_stream)
+    if rc != TA_OK:
+        raise TileAttnError(rc, ta_status_string(rc))
+    return out

@@ -222,3 +222,23 @@ def test_mla_workspace_and_heuristic():
             assert n <= tiles // 8 and (n - 1) * wg < 256
         else:
             assert tiles // 8 <= 1
+
+
+# gemm_bf16: argument errors before any HIP call (fake pointers)
+GA, GB, GC = 0x10000000, 0x30000000, 0x50000000
+GEMM_OK = dict(A=GA, B=GB, C=GC, c_bf16=0, M=256, N=256, K=128, stream=None)
+BAD_GEMM = [
+    (dict(A=0), 1), (dict(B=0), 1), (dict(C=0), 1),
+    (dict(M=0), 2), (dict(N=-1), 2), (dict(K=0), 2),
+    (dict(M=200), 3), (dict(N=100), 3), (dict(K=96), 3),
+    (dict(A=GA + 8), 4), (dict(C=GC + 4), 4),
+    (dict(C=GA + 1024), 6), (dict(C=GB - 4096), 6), (dict(c_bf16=1, C=GB - 256 * 256 * 2 + 16), 6),
+]
+
+
+@no_gpu
+@pytest.mark.parametrize("change,status", BAD_GEMM, ids=[str(c) for c, _ in BAD_GEMM])
+def test_gemm_validation_before_any_hip_call(change, status):
+    a = dict(GEMM_OK, **change)
+    rc = ta.gemm_bf16_raw(a["A"], a["B"], a["C"], a["c_bf16"], a["M"], a["N"], a["K"], a["stream"])
+    assert rc == status, f"{change}: got {ta.STATUS.get(rc, rc)}, want {ta.STATUS[status]}"

@@ -1,0 +1,92 @@
+"""GPU parity of gemm_bf16 (C = A B, bf16 inputs, fp32 accumulation) through
+the C ABI against the float64 oracle.  Tolerance per element, from the
+arithmetic: every bf16 x bf16 product is exact in fp32 and the K-sum is
+accumulated in fp32, so |C - C_ref| <= 1e-5 * sum_k |a_ik||b_kj| (a random
+rounding walk over K/16 accumulation steps stays two orders of magnitude
+below this; a dropped or doubled 16-product step does not); bf16 output adds
+its rounding, 2^-8 |C_ref|."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2504_17577_amd import gen
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+REL_ABS = 1e-5
+
+
+@pytest.fixture(scope="module")
+def ta():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2504_17577_amd import tileattn
+    tileattn.lib()
+    return tileattn
+
+
+def dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def check(tag, c, a, b, rows=None, bf16=False):
+    ref = oracle.gemm(a, b, rows=rows)
+    scale = oracle.gemm_abs(a, b, rows=rows)
+    got = c.float().cpu().numpy() if rows is None else c.float()[torch.tensor(rows)].cpu().numpy()
+    tol = REL_ABS * scale + (2.0 ** -8 * np.abs(ref) if bf16 else 0.0)
+    err = np.abs(got - ref)
+    assert np.isfinite(got).all(), f"{tag}: non-finite output"
+    worst = float((err / tol).max())
+    print(f"{tag}: max|dC|={err.max():.3e}, worst err/tol={worst:.3f}", flush=True)
+    assert worst <= 1.0, tag
+
+
+SHAPES = [(128, 128, 64), (256, 256, 64), (256, 384, 192), (512, 768, 320), (384, 128, 1024)]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=[str(s) for s in SHAPES])
+def test_gemm_full_compare(ta, shape):
+    M, N, K = shape
+    print(f"gemm {shape}", flush=True)
+    a, b = gen.random_gemm_problem(M, N, K, seed=M + N + K)
+    c = torch.full((M, N), float("nan"), device="cuda")
+    ta.gemm_bf16(dev(a), dev(b), out=c)
+    torch.cuda.synchronize()
+    check(f"gemm {shape}", c, a, b)
+
+
+@pytest.mark.parametrize("name", ["gemm_m0", "gemm_m5", "gemm_m3"])
+def test_gemm_workload_sampled(ta, name):
+    """The paper's shapes at full size (both tile configurations): sampled
+    rows against the oracle, every element finite."""
+    w = gen.GEMM_WORKLOADS[name]
+    print(f"gemm workload {name} {w.describe()}", flush=True)
+    a, b = gen.make_gemm_inputs(w, seed=0)
+    c = torch.full((w.M, w.N), float("nan"), device="cuda")
+    ta.gemm_bf16(dev(a), dev(b), out=c)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(c).all())
+    rng = np.random.default_rng(1)
+    rows = sorted({0, 1, 31, 32, 127, 128, 255, 256, w.M - 1} |
+                  {int(x) for x in rng.integers(0, w.M, size=24)})
+    check(f"gemm {name}", c, a, b, rows=rows)
+
+
+def test_gemm_bf16_out_is_rounded_fp32_and_deterministic(ta):
+    a, b = gen.random_gemm_problem(512, 512, 256, seed=9)
+    da, db = dev(a), dev(b)
+    c32 = ta.gemm_bf16(da, db)
+    c32b = ta.gemm_bf16(da, db)
+    c16 = ta.gemm_bf16(da, db, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert torch.equal(c32.view(torch.int32), c32b.view(torch.int32))
+    assert torch.equal(c16.view(torch.int16), c32.to(torch.bfloat16).view(torch.int16))
+    check("gemm bf16 out", c16, a, b, bf16=True)
+
+
+def test_gemm_rejects_bad_shapes(ta):
+    a, b = gen.random_gemm_problem(128, 128, 96, seed=1)
+    with pytest.raises(ta.TileAttnError) as e:
+        ta.gemm_bf16(dev(a), dev(b))
+    assert e.value.status == 3
