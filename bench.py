@@ -335,10 +335,12 @@ def bench_gemm(args, torch, tileattn):
         "check": {"worst_err_over_tol": worst, "rows": len(rows)},
     }
     if not args.no_cpu_baseline:
-        # fp64 oracle on a bounded number of rows (about 10 s)
-        t0 = time.perf_counter()
+        # fp64 oracle on a bounded number of rows (about 10 s), calibrated on
+        # 16 rows after one untimed call (the first call pays numpy's set-up)
         oracle.gemm(a, b, rows=[0])
-        t1 = max(time.perf_counter() - t0, 1e-6)
+        t0 = time.perf_counter()
+        oracle.gemm(a, b, rows=list(range(16)))
+        t1 = max(time.perf_counter() - t0, 1e-6) / 16
         n = int(max(1, min(w.M, 10.0 / t1)))
         t0 = time.perf_counter()
         oracle.gemm(a, b, rows=list(range(n)))
