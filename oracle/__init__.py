@@ -7,7 +7,9 @@ product: inputs arrive as bfloat16 bit arrays from the seeded generator.
 
 The arithmetic lives in ``attn_oracle.c``: the plain softmax-attention
 definition, row by row, in double precision (bottom-right causal alignment,
-grouped-query head map h -> h // (Hq/Hkv), LSE as a natural log).
+grouped-query head map h -> h // (Hq/Hkv), LSE as a natural log).  The MLA
+decode and GEMM references below reduce to that code or to a float64 matmul;
+the Mamba-2 SSD chunk functions are in ``oracle.ssd`` (numpy, float64).
 """
 from __future__ import annotations
 

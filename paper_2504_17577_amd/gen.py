@@ -284,3 +284,123 @@ def make_gemm_inputs(w: GemmWorkload, seed: int = 0):
 
 def random_gemm_problem(M: int, N: int, K: int, seed: int, wid: int = 102):
     return make_gemm_inputs(GemmWorkload("adhoc", wid, M, N, K), seed)
+
+
+# ---------------------------------------------------------------------------
+# Mamba-2 state-space duality (SSD) chunk kernels, the paper's linear-attention
+# workload ("chunk-scan and chunk-state functions from Mamba-2"; appendix
+# table "Linear Attention shapes in our benchmark": batch, 64 heads, sequence
+# length, head dim 64, state dim 128).  Layouts are Mamba-2's:
+#   x      [B, L, H, P]  bf16     per-head input
+#   Bm, Cm [B, L, G, N]  bf16     input / output projections, head h uses group h // (H/G)
+#   dt     [B, L, H]     fp32     step sizes (> 0)
+#   A      [H]           fp32     decay rates (< 0)
+#   D      [H]           fp32     skip weights
+# Recipe: x, Bm, Cm i.i.d. N(0,1); dt = exp(U(ln 1e-3, ln 1e-1)) and
+# A = -exp(U(ln 1, ln 16)), the ranges Mamba-2 initialises them in;
+# D ~ U(0.5, 1.5).  The chunk-scan function also takes the per-chunk matrix
+# cb [B, nc, G, Q, Q] and the entering states [B, nc, H, P, N] (fp32); for
+# tests of that function alone they are drawn here too: cb ~ N(0, N) (the
+# spread of a dot product of two N-vectors of unit normals), states ~ N(0, 1).
+
+TENSOR_X, TENSOR_BM, TENSOR_CM, TENSOR_DT, TENSOR_A, TENSOR_D = 10, 11, 12, 13, 14, 15
+TENSOR_CB, TENSOR_STATES = 16, 17
+
+
+@dataclasses.dataclass(frozen=True)
+class SsdWorkload:
+    """One SSD chunk-kernel problem: shapes and input recipe."""
+
+    name: str
+    wid: int
+    B: int
+    L: int
+    H: int
+    G: int = 1
+    P: int = 64
+    N: int = 128
+    Q: int = 256      # chunk size (Mamba-2's default)
+
+    @property
+    def nc(self) -> int:
+        return -(-self.L // self.Q)
+
+    def flops_state(self) -> int:
+        """Matmul flops of the chunk-state function: 2 P N per position and head."""
+        return 2 * self.B * self.H * self.L * self.P * self.N
+
+    def flops_scan(self) -> int:
+        """Matmul flops of the chunk-scan function per position and head: the
+        entering-state term (2 N P) and the causal within-chunk term
+        (2 P per visible earlier position of the chunk)."""
+        pairs = 0
+        for c in range(self.nc):
+            n = min(self.Q, self.L - c * self.Q)
+            pairs += n * (n + 1) // 2
+        return self.B * self.H * (2 * self.L * self.N * self.P + 2 * pairs * self.P)
+
+    def bytes_state(self) -> int:
+        """Algorithmic HBM bytes of chunk-state: x, Bm, dt read once, fp32 states written."""
+        return (2 * self.B * self.L * (self.H * self.P + self.G * self.N) + 4 * self.B * self.L * self.H
+                + 4 * self.B * self.nc * self.H * self.P * self.N)
+
+    def bytes_scan(self) -> int:
+        """Algorithmic HBM bytes of chunk-scan: x, Cm, cb (lower triangle is all
+        that is needed, counted whole), dt, entering states read once; fp32 out written."""
+        return (2 * self.B * self.L * (self.H * self.P + self.G * self.N)
+                + 4 * self.B * self.nc * self.G * self.Q * self.Q + 4 * self.B * self.L * self.H
+                + 4 * self.B * self.nc * self.H * self.P * self.N + 4 * self.B * self.L * self.H * self.P)
+
+    def describe(self) -> str:
+        return (f"B={self.B} L={self.L} H={self.H} G={self.G} P={self.P} N={self.N} "
+                f"chunk={self.Q}")
+
+
+SSD_WORKLOADS = {
+    w.name: w
+    for w in (
+        SsdWorkload("ssd_tiny_s300", 50, 2, 300, 4, 2),
+        SsdWorkload("ssd_b1_s1k", 51, 1, 1024, 64),
+        SsdWorkload("ssd_b1_s2k", 52, 1, 2048, 64),
+        SsdWorkload("ssd_b1_s8k", 53, 1, 8192, 64),
+        SsdWorkload("ssd_b64_s1k", 54, 64, 1024, 64),
+        SsdWorkload("ssd_b64_s2k", 55, 64, 2048, 64),
+        SsdWorkload("ssd_b64_s8k", 56, 64, 8192, 64),
+    )
+}
+
+
+def _uniform_f32(shape, lo, hi, seed, wid, tensor):
+    g = _stream(seed, wid, tensor)
+    return g.uniform(lo, hi, size=int(np.prod(shape))).astype(np.float32).reshape(shape)
+
+
+def make_ssd_inputs(w: SsdWorkload, seed: int = 0):
+    """dict of x, Bm, Cm (bfloat16 bits), dt, A, D (float32) for workload ``w``."""
+    ln = math.log
+    return {
+        "x": normal_bf16((w.B, w.L, w.H, w.P), seed, w.wid, TENSOR_X),
+        "Bm": normal_bf16((w.B, w.L, w.G, w.N), seed, w.wid, TENSOR_BM),
+        "Cm": normal_bf16((w.B, w.L, w.G, w.N), seed, w.wid, TENSOR_CM),
+        "dt": np.exp(_uniform_f32((w.B, w.L, w.H), ln(1e-3), ln(1e-1), seed, w.wid, TENSOR_DT)),
+        "A": -np.exp(_uniform_f32((w.H,), ln(1.0), ln(16.0), seed, w.wid, TENSOR_A)),
+        "D": _uniform_f32((w.H,), 0.5, 1.5, seed, w.wid, TENSOR_D),
+    }
+
+
+def make_ssd_scan_extras(w: SsdWorkload, seed: int = 0):
+    """(cb [B,nc,G,Q,Q], states [B,nc,H,P,N]) float32 draws for testing the
+    chunk-scan function on its own."""
+    g = _stream(seed, w.wid, TENSOR_CB)
+    cb = g.standard_normal(size=w.B * w.nc * w.G * w.Q * w.Q, dtype=np.float32)
+    cb = (cb * np.float32(math.sqrt(w.N))).reshape(w.B, w.nc, w.G, w.Q, w.Q)
+    g = _stream(seed, w.wid, TENSOR_STATES)
+    st = g.standard_normal(size=w.B * w.nc * w.H * w.P * w.N, dtype=np.float32)
+    return cb, st.reshape(w.B, w.nc, w.H, w.P, w.N)
+
+
+def random_ssd_problem(B, L, H, G, seed: int, P: int = 64, N: int = 128, Q: int = 256,
+                       wid: int = 103):
+    """(workload, inputs) for an ad-hoc SSD shape (tests' edge cases)."""
+    w = SsdWorkload("adhoc", wid, B, L, H, G, P, N, Q)
+    return w, make_ssd_inputs(w, seed)
