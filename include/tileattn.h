@@ -189,6 +189,62 @@ ta_status gemm_bf16(const void *A, const void *B, void *C, int c_bf16, int M, in
                     void *stream);
 
 /*
+ * Mamba-2 state-space-duality (SSD) chunk functions: the paper's linear
+ * attention workload ("chunk-scan and chunk-state functions from Mamba-2",
+ * Section "Numerical Experiments", paragraph "Linear Attention Performance";
+ * shapes in the appendix table "Linear Attention shapes in our benchmark").
+ * For batch b, head h (group g = h / (nheads / ngroups)) and chunk c of
+ * chunk_size positions, with a_l = sum_{l' <= l} dt_{l'} A_h the cumulative
+ * log-decay inside the chunk (each call forms it from dt and A itself):
+ *   ssd_chunk_state    S_c[p][n] = sum_l exp(a_last - a_l) dt_l x_l[p] Bm_l[n]
+ *   ssd_state_passing  H_c = exp(a_last(c)) H_{c-1} + S_c, H_{-1} = 0; writes
+ *                      the state each chunk enters with, H_{c-1}
+ *   ssd_bmm_chunk      cb[l][s] = Cm_l . Bm_s (both positions in chunk c)
+ *   ssd_chunk_scan     y_l[p] = exp(a_l) sum_n H_{c-1}[p][n] Cm_l[n]
+ *                             + sum_{s <= l} cb[l][s] exp(a_l - a_s) dt_s x_s[p]
+ *                             + D_h x_l[p]
+ * Chained, they give the output of the recurrence h_t = exp(dt_t A) h_{t-1} +
+ * dt_t x_t Bm_t^T, y_t = h_t Cm_t + D x_t (Mamba-2, "Transformers are SSMs").
+ *
+ * Layouts (contiguous, row-major; L = seqlen, nc = ceil(L / chunk_size)):
+ *   x       device, bf16 [batch, L, nheads, headdim]
+ *   Bm, Cm  device, bf16 [batch, L, ngroups, dstate]
+ *   dt      device, fp32 [batch, L, nheads]           step sizes (> 0)
+ *   A       device, fp32 [nheads]                     decay rates (<= 0)
+ *   D       device, fp32 [nheads], or NULL for no skip term
+ *   cb      device, fp32 [batch, nc, ngroups, chunk_size, chunk_size]
+ *   states, prev_states
+ *           device, fp32 [batch, nc, nheads, headdim, dstate]
+ *   final_states device, fp32 [batch, nheads, headdim, dstate], or NULL
+ *   out     device, fp32 [batch, L, nheads, headdim]
+ * A last chunk shorter than chunk_size is handled as if padded with dt = 0
+ * and zero x, Bm, Cm: padded positions add nothing (cb rows and columns of
+ * padded positions are written as zero; out rows past L are not written).
+ * headdim == 64, dstate == 128, chunk_size == 256 (else TA_ERR_UNSUPPORTED);
+ * nheads % ngroups == 0 (else TA_ERR_INVALID_SHAPE).  bf16 and output
+ * pointers 16-byte aligned, fp32 vectors 4-byte aligned (TA_ERR_MISALIGNED);
+ * outputs must not overlap inputs (TA_ERR_ALIASING).  The decay- and
+ * dt-weighted operand of each contraction (and, in the chunk scan, the fp32
+ * entering state) is rounded to bf16 before the bf16 x bf16 -> fp32 MFMA.
+ * Ownership, asynchrony and error behaviour as attn_fwd.
+ */
+ta_status ssd_chunk_state(const void *x, const void *Bm, const float *dt, const float *A,
+                          float *states, int batch, int seqlen, int nheads, int ngroups,
+                          int headdim, int dstate, int chunk_size, void *stream);
+
+ta_status ssd_state_passing(const float *states, const float *dt, const float *A,
+                            float *prev_states, float *final_states, int batch, int seqlen,
+                            int nheads, int headdim, int dstate, int chunk_size, void *stream);
+
+ta_status ssd_bmm_chunk(const void *Cm, const void *Bm, float *cb, int batch, int seqlen,
+                        int ngroups, int dstate, int chunk_size, void *stream);
+
+ta_status ssd_chunk_scan(const void *x, const void *Cm, const float *cb, const float *dt,
+                         const float *A, const float *prev_states, const float *D, float *out,
+                         int batch, int seqlen, int nheads, int ngroups, int headdim,
+                         int dstate, int chunk_size, void *stream);
+
+/*
  * ta_schedule — host-side tile schedule of attn_fwd, for tests and tools.
  * For the query tile `q_tile` (rows q_tile*BM .. q_tile*BM+BM-1, BM from
  * ta_tile_shape) it reports how many key tiles of BN keys the kernel visits

@@ -7,7 +7,7 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SOURCES = [os.path.join(PKG, "csrc", n) for n in ("attn_fwd.hip", "mla_decode.hip", "gemm.hip")]
+SOURCES = [os.path.join(PKG, "csrc", n) for n in ("attn_fwd.hip", "mla_decode.hip", "gemm.hip", "ssd.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libtileattn.so")
 

@@ -1,0 +1,644 @@
+// Mamba-2 state-space-duality (SSD) chunk kernels for gfx950 (MI355X): the
+// chunk-state and chunk-scan functions the paper benchmarks as its linear
+// attention workload (Section "Numerical Experiments", paragraph "Linear
+// Attention Performance"; shapes in the appendix table "Linear Attention
+// shapes in our benchmark"), plus the state passing and per-chunk C B^T
+// steps that complete the chained forward pass.
+//
+// For batch b, head h (group g = h / (H/G)) and chunk c of Q = 256 positions,
+// with the cumulative log-decay a_l = sum_{l' <= l} dt_{l'} A_h inside the
+// chunk:
+//   chunk state    S_c[p][n]  = sum_l exp(a_last - a_l) dt_l x_l[p] Bm_l[n]
+//   state passing  H_c = exp(a_last(c)) H_{c-1} + S_c, H_{-1} = 0; chunk c
+//                  enters with H_{c-1}
+//   chunk matrix   cb[l][s]   = Cm_l . Bm_s
+//   chunk scan     y_l[p] = exp(a_l) sum_n H_{c-1}[p][n] Cm_l[n]
+//                         + sum_{s <= l} cb[l][s] exp(a_l - a_s) dt_s x_s[p]
+//                         + D_h x_l[p]
+// The design is this library's own for CDNA4:
+//  * One workgroup of four wave64s per (batch, chunk, head).  The workgroup
+//    forms the chunk's cumulative decay itself (a 256-wide prefix sum of
+//    dt * A), so the functions take the raw dt and A.
+//  * Every contraction runs on v_mfma_f32_32x32x16_bf16 with fp32
+//    accumulation.  The decay- and dt-weighted operand (x for the chunk
+//    state, the masked cb matrix for the chunk scan) and the fp32 entering
+//    state are rounded to bf16 (nearest even) once, right before the MFMA.
+//  * Outputs are computed transposed (S^T, y^T), so that each lane of the
+//    32x32 accumulator layout owns four consecutive elements of a row of the
+//    row-major result and stores them as one 16-byte write.
+//  * Operands that must be read along the sequence (columns of x and Bm)
+//    come from LDS through the gfx950 transpose read ds_read_b64_tr_b16;
+//    rows are read with ds_read_b128 or straight from global memory.
+//  * Workgroup ids are remapped so that each XCD runs whole (batch, chunk)
+//    groups of heads: the chunk's Bm, Cm and cb, shared by all its heads,
+//    stay in that XCD's L2.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "tileattn.h"
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+constexpr int SQ = 256;       // chunk length
+constexpr int SP = 64;        // head dim
+constexpr int SN = 128;       // state dim
+constexpr int NT = 256;       // threads per workgroup
+constexpr int NXCD = 8;
+constexpr float LOG2E = 1.44269504088896340736f;
+
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c)
+{
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// hardware workgroup id -> logical id: XCD x (which receives ids x, x + 8,
+// ...) gets the contiguous logical range [x * per, ...)
+__device__ __forceinline__ int xcd_logical(int bid, int n_wg)
+{
+    const int per = n_wg / NXCD, rem = n_wg % NXCD;
+    const int xcd = bid % NXCD, idx = bid / NXCD;
+    return xcd * per + (xcd < rem ? xcd : rem) + idx;
+}
+
+// inclusive prefix sum over the workgroup's 256 threads (ascending tid)
+__device__ float block_scan(float v, float *wsum)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const float u = __shfl_up(v, d, 64);
+        if (lane >= d)
+            v += u;
+    }
+    if (lane == 63)
+        wsum[wave] = v;
+    __syncthreads();
+    float off = 0.f;
+    for (int w = 0; w < wave; ++w)
+        off += wsum[w];
+    return v + off;
+}
+
+// 16-byte chunk c of row r of a tile with 256-byte rows (128 bf16), stored
+// at c ^ swz: conflict-free for the transpose reads (4 rows x 64 bytes per
+// half wave) and for 32-row ds_read_b128 operand reads
+__device__ __forceinline__ int swz_tr256(int r) { return 4 * (r & 3); }
+__device__ __forceinline__ int swz_row256(int r) { return r & 15; }
+// 128-byte rows (64 bf16)
+__device__ __forceinline__ int swz_tr128(int r) { return 4 * ((r >> 1) & 1); }
+
+// Transpose read of an MFMA operand from a row-major bf16 tile: lane l gets
+// the 8 k-slots {k0 + 4h + t, k0 + 8 + 4h + t : t < 4} (h = l / 32) of
+// column col0 + l % 32.  Two ds_read_b64_tr_b16: each group of 16 lanes reads
+// a 4 x 16 block (rows k0 + 4h (+8) + s/4, columns col0 + 16((l>>4)&1) +
+// 4(s&3) for s = l % 16) and the transpose hands lane s column s of it.
+template <int ROWB, int (*SWZ)(int)>
+__device__ __forceinline__ bf16x8 tr_operand(const unsigned char *tile, int k0, int col0, int lane)
+{
+    const int gq = lane >> 4, sl = lane & 15, h = lane >> 5;
+    const int r0 = k0 + 4 * h + (sl >> 2), r1 = r0 + 8;
+    const int col = col0 + 16 * (gq & 1) + 4 * (sl & 3);
+    const int bin = (2 * col) & 15;
+    const unsigned char *p0 = tile + r0 * ROWB + (((col >> 3) ^ SWZ(r0)) * 16) + bin;
+    const unsigned char *p1 = tile + r1 * ROWB + (((col >> 3) ^ SWZ(r1)) * 16) + bin;
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p0);
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p1);
+    const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+    return __builtin_bit_cast(bf16x8, u32x4{l2[0], l2[1], h2[0], h2[1]});
+}
+
+struct SsdShape {
+    int B, L, H, G, nc;
+    int hpg;   // H / G
+};
+
+// ---------------------------------------------------------------------------
+// chunk state: S^T[n][p] = sum_l Bm_l[n] (x_l[p] w_l),  w_l = exp(a_last - a_l) dt_l
+
+struct StateArgs {
+    SsdShape s;
+    const uint16_t *x, *Bm;
+    const float *dt, *A;
+    float *states;
+};
+
+__global__ __launch_bounds__(NT, 2) void chunk_state_kernel(StateArgs args)
+{
+    const StateArgs &a = args;
+    constexpr int HALF = SQ / 2;   // positions staged per pass
+    __shared__ __attribute__((aligned(16))) unsigned char bt[HALF * SN * 2];   // Bm rows, 32 KB
+    __shared__ __attribute__((aligned(16))) unsigned char xt[HALF * SP * 2];   // weighted x rows, 16 KB
+    __shared__ float wts[SQ];
+    __shared__ float wsum[4];
+    __shared__ float alast;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int n_wg = a.s.B * a.s.nc * a.s.H;
+    const int logical = xcd_logical(blockIdx.x, n_wg);
+    const int h = logical % a.s.H;
+    const int c = (logical / a.s.H) % a.s.nc;
+    const int b = logical / (a.s.H * a.s.nc);
+    const int g = h / a.s.hpg;
+
+    // cumulative log-decay of this chunk and the per-position weights
+    const int t = c * SQ + tid;
+    const float dtl = t < a.s.L ? a.dt[((size_t)b * a.s.L + t) * a.s.H + h] : 0.f;
+    const float cum = block_scan(dtl * a.A[h], wsum);
+    if (tid == NT - 1)
+        alast = cum;
+    __syncthreads();
+    const float a_last = alast;
+    wts[tid] = exp2f((a_last - cum) * LOG2E) * dtl;
+
+    f32x16 acc[2];
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            acc[pb][r] = 0.f;
+
+    const size_t brow = (size_t)a.s.G * SN;          // Bm elements per position
+    const size_t xrow = (size_t)a.s.H * SP;          // x elements per position
+    for (int half = 0; half < 2; ++half) {
+        __syncthreads();   // wts visible; previous pass's reads done
+        const int p0 = c * SQ + half * HALF;
+        // Bm: 128 rows x 16 chunks of 16 bytes
+#pragma unroll
+        for (int i = 0; i < HALF * 16 / NT; ++i) {
+            const int q = i * NT + tid, r = q >> 4, cc = q & 15;
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if (p0 + r < a.s.L)
+                v = *(const u32x4 *)(a.Bm + ((size_t)b * a.s.L + p0 + r) * brow + (size_t)g * SN + cc * 8);
+            *(u32x4 *)(bt + r * (SN * 2) + ((cc ^ swz_tr256(r)) * 16)) = v;
+        }
+        // x: 128 rows x 8 chunks, each scaled by its position's weight
+#pragma unroll
+        for (int i = 0; i < HALF * 8 / NT; ++i) {
+            const int q = i * NT + tid, r = q >> 3, cc = q & 7;
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if (p0 + r < a.s.L) {
+                const u32x4 u = *(const u32x4 *)(a.x + ((size_t)b * a.s.L + p0 + r) * xrow +
+                                                 (size_t)h * SP + cc * 8);
+                const float w = wts[half * HALF + r];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    v[e] = pack_bf16(bf16_lo(u[e]) * w, bf16_hi(u[e]) * w);
+            }
+            *(u32x4 *)(xt + r * (SP * 2) + ((cc ^ swz_tr128(r)) * 16)) = v;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int ks = 0; ks < HALF / 16; ++ks) {
+            const bf16x8 av = tr_operand<SN * 2, swz_tr256>(bt, 16 * ks, 32 * wave, lane);
+#pragma unroll
+            for (int pb = 0; pb < 2; ++pb) {
+                const bf16x8 bv = tr_operand<SP * 2, swz_tr128>(xt, 16 * ks, 32 * pb, lane);
+                acc[pb] = mfma32(av, bv, acc[pb]);
+            }
+        }
+    }
+
+    // lane holds S^T[n][p] for p = 32 pb + lane % 32 and n = 32 wave + 8 j +
+    // 4 (lane / 32) + 0..3: four consecutive n of row p of S
+    float *out = a.states + (((size_t)b * a.s.nc + c) * a.s.H + h) * (SP * SN);
+    const int col = lane & 31, hl = lane >> 5;
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int p = 32 * pb + col, n = 32 * wave + 8 * j + 4 * hl;
+            *(float4 *)(out + p * SN + n) =
+                float4{acc[pb][4 * j], acc[pb][4 * j + 1], acc[pb][4 * j + 2], acc[pb][4 * j + 3]};
+        }
+}
+
+// ---------------------------------------------------------------------------
+// chunk scan: y^T[p][l] = exp(a_l) sum_n Hin[p][n] Cm_l[n]
+//                         + sum_{s <= l} x_s[p] (cb[l][s] exp(a_l - a_s) dt_s)  + D x_l[p]
+
+struct ScanArgs {
+    SsdShape s;
+    const uint16_t *x, *Cm;
+    const float *cb, *dt, *A, *prev, *D;
+    float *out;
+};
+
+__global__ __launch_bounds__(NT, 2) void chunk_scan_kernel(ScanArgs args)
+{
+    const ScanArgs &a = args;
+    __shared__ __attribute__((aligned(16))) unsigned char xt[SQ * SP * 2];    // x rows, 32 KB
+    __shared__ __attribute__((aligned(16))) unsigned char ht[SP * SN * 2];    // Hin (bf16), 16 KB
+    __shared__ __attribute__((aligned(16))) float a2s[SQ];                    // log2-domain a_l
+    __shared__ __attribute__((aligned(16))) float g2s[SQ];                    // a2_s - log2(dt_s)
+    __shared__ float wsum[4];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int n_wg = a.s.B * a.s.nc * a.s.H;
+    const int logical = xcd_logical(blockIdx.x, n_wg);
+    const int h = logical % a.s.H;
+    const int c = (logical / a.s.H) % a.s.nc;
+    const int b = logical / (a.s.H * a.s.nc);
+    const int g = h / a.s.hpg;
+    const int t0 = c * SQ;
+
+    const int t = t0 + tid;
+    const bool valid = t < a.s.L;
+    const float dtl = valid ? a.dt[((size_t)b * a.s.L + t) * a.s.H + h] : 0.f;
+    const float a2 = block_scan(dtl * a.A[h], wsum) * LOG2E;
+    a2s[tid] = a2;
+    g2s[tid] = valid ? a2 - log2f(dtl) : INFINITY;   // padded positions weigh zero
+
+    // stage x (256 rows x 8 chunks) and the entering state as bf16 (64 rows
+    // x 16 chunks, each from 8 fp32)
+    const size_t xrow = (size_t)a.s.H * SP;
+#pragma unroll
+    for (int i = 0; i < SQ * 8 / NT; ++i) {
+        const int q = i * NT + tid, r = q >> 3, cc = q & 7;
+        u32x4 v = {0u, 0u, 0u, 0u};
+        if (t0 + r < a.s.L)
+            v = *(const u32x4 *)(a.x + ((size_t)b * a.s.L + t0 + r) * xrow + (size_t)h * SP + cc * 8);
+        *(u32x4 *)(xt + r * (SP * 2) + ((cc ^ swz_tr128(r)) * 16)) = v;
+    }
+    const float *hin = a.prev + (((size_t)b * a.s.nc + c) * a.s.H + h) * (SP * SN);
+#pragma unroll
+    for (int i = 0; i < SP * 16 / NT; ++i) {
+        const int q = i * NT + tid, r = q >> 4, cc = q & 15;
+        const float4 f0 = *(const float4 *)(hin + r * SN + cc * 8);
+        const float4 f1 = *(const float4 *)(hin + r * SN + cc * 8 + 4);
+        const u32x4 v = {pack_bf16(f0.x, f0.y), pack_bf16(f0.z, f0.w), pack_bf16(f1.x, f1.y),
+                         pack_bf16(f1.z, f1.w)};
+        *(u32x4 *)(ht + r * (SN * 2) + ((cc ^ swz_row256(r)) * 16)) = v;
+    }
+    __syncthreads();
+
+    const int col = lane & 31, hl = lane >> 5;
+    // this wave's 32-position blocks: {wave, 7 - wave} (balances the causal work)
+    const int lbs[2] = {wave, 7 - wave};
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[i][pb][r] = 0.f;
+
+    // entering state: A = Hin rows (p), B = Cm rows (l), k = n
+    const size_t crow = (size_t)a.s.G * SN;
+#pragma unroll
+    for (int ks = 0; ks < SN / 16; ++ks) {
+        bf16x8 av[2], bv[2];
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb) {
+            const int r = 32 * pb + col;
+            av[pb] = *(const bf16x8 *)(ht + r * (SN * 2) + (((2 * ks + hl) ^ swz_row256(r)) * 16));
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int tl = t0 + 32 * lbs[i] + col;
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if (tl < a.s.L)
+                v = *(const u32x4 *)(a.Cm + ((size_t)b * a.s.L + tl) * crow + (size_t)g * SN +
+                                     16 * ks + 8 * hl);
+            bv[i] = __builtin_bit_cast(bf16x8, v);
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int pb = 0; pb < 2; ++pb)
+                acc[i][pb] = mfma32(av[pb], bv[i], acc[i][pb]);
+    }
+    // decay the entering state to each position (lane's column l)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const float e = exp2f(a2s[32 * lbs[i] + col]);
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[i][pb][r] *= e;
+    }
+
+    // within the chunk: A = x^T (p, s) by transpose reads, B = the weighted
+    // cb row of position l, k = s <= l
+    const float *cbm = a.cb + (((size_t)b * a.s.nc + c) * a.s.G + g) * (SQ * SQ);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int lb = lbs[i];
+        const int l = 32 * lb + col;
+        const float a2l = a2s[l];
+        const float *cbr = cbm + (size_t)l * SQ;
+        for (int ks = 0; ks <= 2 * lb + 1; ++ks) {
+            const int s_lo = 16 * ks + 4 * hl, s_hi = s_lo + 8;
+            const float4 c0 = *(const float4 *)(cbr + s_lo);
+            const float4 c1 = *(const float4 *)(cbr + s_hi);
+            const float4 q0 = *(const float4 *)(g2s + s_lo);
+            const float4 q1 = *(const float4 *)(g2s + s_hi);
+            float m[8] = {c0.x * exp2f(a2l - q0.x), c0.y * exp2f(a2l - q0.y),
+                          c0.z * exp2f(a2l - q0.z), c0.w * exp2f(a2l - q0.w),
+                          c1.x * exp2f(a2l - q1.x), c1.y * exp2f(a2l - q1.y),
+                          c1.z * exp2f(a2l - q1.z), c1.w * exp2f(a2l - q1.w)};
+            if (ks >= 2 * lb) {   // blocks crossing the diagonal: keep s <= l
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    m[e] = s_lo + e <= l ? m[e] : 0.f;
+                    m[4 + e] = s_hi + e <= l ? m[4 + e] : 0.f;
+                }
+            }
+            const bf16x8 bv = __builtin_bit_cast(
+                bf16x8, u32x4{pack_bf16(m[0], m[1]), pack_bf16(m[2], m[3]), pack_bf16(m[4], m[5]),
+                              pack_bf16(m[6], m[7])});
+#pragma unroll
+            for (int pb = 0; pb < 2; ++pb) {
+                const bf16x8 av = tr_operand<SP * 2, swz_tr128>(xt, 16 * ks, 32 * pb, lane);
+                acc[i][pb] = mfma32(av, bv, acc[i][pb]);
+            }
+        }
+    }
+
+    // skip term and store: lane holds y^T[p][l] for l = 32 lb + col and
+    // p = 32 pb + 8 j + 4 hl + 0..3 (four consecutive p of output row l)
+    const float dh = a.D ? a.D[h] : 0.f;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int l = 32 * lbs[i] + col;
+        if (t0 + l >= a.s.L)
+            continue;
+        float *yo = a.out + ((size_t)b * a.s.L + t0 + l) * xrow + (size_t)h * SP;
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int p = 32 * pb + 8 * j + 4 * hl;
+                const u32x2 xv = *(const u32x2 *)(xt + l * (SP * 2) + (((p >> 3) ^ swz_tr128(l)) * 16) +
+                                                  (2 * p & 15));
+                *(float4 *)(yo + p) = float4{acc[i][pb][4 * j] + dh * bf16_lo(xv[0]),
+                                             acc[i][pb][4 * j + 1] + dh * bf16_hi(xv[0]),
+                                             acc[i][pb][4 * j + 2] + dh * bf16_lo(xv[1]),
+                                             acc[i][pb][4 * j + 3] + dh * bf16_hi(xv[1])};
+            }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// chunk matrix: cb^T[s][l] = sum_n Bm_s[n] Cm_l[n], eight waves, wave w owns
+// the 32 rows s of block w and all 256 columns l
+
+struct BmmArgs {
+    SsdShape s;
+    const uint16_t *Cm, *Bm;
+    float *cb;
+};
+
+__global__ __launch_bounds__(512, 1) void bmm_chunk_kernel(BmmArgs args)
+{
+    const BmmArgs &a = args;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int n_wg = a.s.B * a.s.nc * a.s.G;
+    const int logical = xcd_logical(blockIdx.x, n_wg);
+    const int g = logical % a.s.G;
+    const int c = (logical / a.s.G) % a.s.nc;
+    const int b = logical / (a.s.G * a.s.nc);
+    const int t0 = c * SQ, col = lane & 31, hl = lane >> 5;
+    const size_t row = (size_t)a.s.G * SN;
+    f32x16 acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            acc[j][r] = 0.f;
+    const int ts = t0 + 32 * wave + col;
+#pragma unroll 2
+    for (int ks = 0; ks < SN / 16; ++ks) {
+        u32x4 va = {0u, 0u, 0u, 0u};
+        if (ts < a.s.L)
+            va = *(const u32x4 *)(a.Bm + ((size_t)b * a.s.L + ts) * row + (size_t)g * SN + 16 * ks + 8 * hl);
+        const bf16x8 av = __builtin_bit_cast(bf16x8, va);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int tl = t0 + 32 * j + col;
+            u32x4 vb = {0u, 0u, 0u, 0u};
+            if (tl < a.s.L)
+                vb = *(const u32x4 *)(a.Cm + ((size_t)b * a.s.L + tl) * row + (size_t)g * SN + 16 * ks +
+                                      8 * hl);
+            acc[j] = mfma32(av, __builtin_bit_cast(bf16x8, vb), acc[j]);
+        }
+    }
+    float *out = a.cb + (((size_t)b * a.s.nc + c) * a.s.G + g) * (SQ * SQ);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int l = 32 * j + col, s = 32 * wave + 8 * q + 4 * hl;
+            *(float4 *)(out + (size_t)l * SQ + s) =
+                float4{acc[j][4 * q], acc[j][4 * q + 1], acc[j][4 * q + 2], acc[j][4 * q + 3]};
+        }
+}
+
+// ---------------------------------------------------------------------------
+// state passing: per (batch, head, quarter of the P x N state), sequential
+// over chunks: prev[c] = H; H = exp(A sum_{l in c} dt_l) H + S_c
+
+struct PassArgs {
+    SsdShape s;
+    const float *states, *dt, *A;
+    float *prev, *final_states;
+};
+
+__global__ __launch_bounds__(NT, 4) void state_passing_kernel(PassArgs args)
+{
+    const PassArgs &a = args;
+    __shared__ float wsum[4];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int qtr = blockIdx.x & 3;
+    const int bh = blockIdx.x >> 2;
+    const int h = bh % a.s.H, b = bh / a.s.H;
+    const int e0 = qtr * (SP * SN / 4) + tid * 8;
+    const float Ah = a.A[h];
+    float4 h0 = {0.f, 0.f, 0.f, 0.f}, h1 = {0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < a.s.nc; ++c) {
+        const int t = c * SQ + tid;
+        float v = t < a.s.L ? a.dt[((size_t)b * a.s.L + t) * a.s.H + h] : 0.f;
+#pragma unroll
+        for (int d = 32; d >= 1; d >>= 1)
+            v += __shfl_xor(v, d, 64);
+        if (lane == 0)
+            wsum[wave] = v;
+        __syncthreads();
+        const float decay = exp2f((wsum[0] + wsum[1] + wsum[2] + wsum[3]) * Ah * LOG2E);
+        __syncthreads();
+        const size_t off = (((size_t)b * a.s.nc + c) * a.s.H + h) * (SP * SN) + e0;
+        *(float4 *)(a.prev + off) = h0;
+        *(float4 *)(a.prev + off + 4) = h1;
+        const float4 s0 = *(const float4 *)(a.states + off);
+        const float4 s1 = *(const float4 *)(a.states + off + 4);
+        h0 = float4{decay * h0.x + s0.x, decay * h0.y + s0.y, decay * h0.z + s0.z, decay * h0.w + s0.w};
+        h1 = float4{decay * h1.x + s1.x, decay * h1.y + s1.y, decay * h1.z + s1.z, decay * h1.w + s1.w};
+    }
+    if (a.final_states) {
+        float *f = a.final_states + ((size_t)b * a.s.H + h) * (SP * SN) + e0;
+        *(float4 *)f = h0;
+        *(float4 *)(f + 4) = h1;
+    }
+}
+
+bool misaligned(const void *p) { return ((uintptr_t)p & 15u) != 0; }
+
+bool overlaps(const void *p, size_t pn, const void *q, size_t qn)
+{
+    if (!p || !q)
+        return false;
+    const uintptr_t x = (uintptr_t)p, y = (uintptr_t)q;
+    return x < y + qn && y < x + pn;
+}
+
+// shared shape validation; fills `s`
+ta_status check_shape(int batch, int seqlen, int nheads, int ngroups, int headdim, int dstate,
+                      int chunk_size, SsdShape &s)
+{
+    if (batch < 1 || seqlen < 1 || nheads < 1 || ngroups < 1 || nheads % ngroups)
+        return TA_ERR_INVALID_SHAPE;
+    if (headdim != SP || dstate != SN || chunk_size != SQ)
+        return TA_ERR_UNSUPPORTED;
+    const int64_t nc = ((int64_t)seqlen + SQ - 1) / SQ;
+    // grid sizes and per-tensor element counts within the kernels' index types
+    if ((int64_t)batch * nc * nheads >= (1ll << 31) || (int64_t)batch * nheads * 4 >= (1ll << 31) ||
+        (int64_t)batch * nc * (nheads > ngroups ? nheads : ngroups) * SQ * SQ >= (1ll << 46))
+        return TA_ERR_INVALID_SHAPE;
+    s.B = batch;
+    s.L = seqlen;
+    s.H = nheads;
+    s.G = ngroups;
+    s.nc = (int)nc;
+    s.hpg = nheads / ngroups;
+    return TA_OK;
+}
+
+ta_status launched(hipError_t e) { return e == hipSuccess ? TA_OK : TA_ERR_LAUNCH; }
+
+}  // namespace
+
+extern "C" {
+
+ta_status ssd_chunk_state(const void *x, const void *Bm, const float *dt, const float *A,
+                          float *states, int batch, int seqlen, int nheads, int ngroups,
+                          int headdim, int dstate, int chunk_size, void *stream)
+{
+    if (!x || !Bm || !dt || !A || !states)
+        return TA_ERR_NULL_POINTER;
+    SsdShape s;
+    const ta_status st = check_shape(batch, seqlen, nheads, ngroups, headdim, dstate, chunk_size, s);
+    if (st != TA_OK)
+        return st;
+    if (misaligned(x) || misaligned(Bm) || misaligned(states) || ((uintptr_t)dt & 3) ||
+        ((uintptr_t)A & 3))
+        return TA_ERR_MISALIGNED;
+    const size_t nx = (size_t)batch * seqlen * nheads * SP * 2, nb = (size_t)batch * seqlen * ngroups * SN * 2;
+    const size_t ns = (size_t)batch * s.nc * nheads * SP * SN * 4;
+    const size_t ndt = (size_t)batch * seqlen * nheads * 4;
+    if (overlaps(states, ns, x, nx) || overlaps(states, ns, Bm, nb) || overlaps(states, ns, dt, ndt) ||
+        overlaps(states, ns, A, (size_t)nheads * 4))
+        return TA_ERR_ALIASING;
+    StateArgs a{s, (const uint16_t *)x, (const uint16_t *)Bm, dt, A, states};
+    hipLaunchKernelGGL(chunk_state_kernel, dim3(s.B * s.nc * s.H), dim3(NT), 0, (hipStream_t)stream, a);
+    return launched(hipGetLastError());
+}
+
+ta_status ssd_chunk_scan(const void *x, const void *Cm, const float *cb, const float *dt,
+                         const float *A, const float *prev_states, const float *D, float *out,
+                         int batch, int seqlen, int nheads, int ngroups, int headdim, int dstate,
+                         int chunk_size, void *stream)
+{
+    if (!x || !Cm || !cb || !dt || !A || !prev_states || !out)
+        return TA_ERR_NULL_POINTER;
+    SsdShape s;
+    const ta_status st = check_shape(batch, seqlen, nheads, ngroups, headdim, dstate, chunk_size, s);
+    if (st != TA_OK)
+        return st;
+    if (misaligned(x) || misaligned(Cm) || misaligned(cb) || misaligned(prev_states) ||
+        misaligned(out) || ((uintptr_t)dt & 3) || ((uintptr_t)A & 3) || ((uintptr_t)D & 3))
+        return TA_ERR_MISALIGNED;
+    const size_t nx = (size_t)batch * seqlen * nheads * SP;
+    const size_t no = nx * 4;
+    const size_t ins[][2] = {
+        {(size_t)x, nx * 2},
+        {(size_t)Cm, (size_t)batch * seqlen * ngroups * SN * 2},
+        {(size_t)cb, (size_t)batch * s.nc * ngroups * SQ * SQ * 4},
+        {(size_t)dt, (size_t)batch * seqlen * nheads * 4},
+        {(size_t)A, (size_t)nheads * 4},
+        {(size_t)prev_states, (size_t)batch * s.nc * nheads * SP * SN * 4},
+        {(size_t)D, D ? (size_t)nheads * 4 : 0},
+    };
+    for (const auto &in : ins)
+        if (overlaps(out, no, (const void *)in[0], in[1]))
+            return TA_ERR_ALIASING;
+    ScanArgs a{s, (const uint16_t *)x, (const uint16_t *)Cm, cb, dt, A, prev_states, D, out};
+    hipLaunchKernelGGL(chunk_scan_kernel, dim3(s.B * s.nc * s.H), dim3(NT), 0, (hipStream_t)stream, a);
+    return launched(hipGetLastError());
+}
+
+ta_status ssd_bmm_chunk(const void *Cm, const void *Bm, float *cb, int batch, int seqlen,
+                        int ngroups, int dstate, int chunk_size, void *stream)
+{
+    if (!Cm || !Bm || !cb)
+        return TA_ERR_NULL_POINTER;
+    SsdShape s;
+    const ta_status st = check_shape(batch, seqlen, ngroups, ngroups, SP, dstate, chunk_size, s);
+    if (st != TA_OK)
+        return st;
+    if (misaligned(Cm) || misaligned(Bm) || misaligned(cb))
+        return TA_ERR_MISALIGNED;
+    const size_t nbc = (size_t)batch * seqlen * ngroups * SN * 2;
+    const size_t ncb = (size_t)batch * s.nc * ngroups * SQ * SQ * 4;
+    if (overlaps(cb, ncb, Cm, nbc) || overlaps(cb, ncb, Bm, nbc))
+        return TA_ERR_ALIASING;
+    BmmArgs a{s, (const uint16_t *)Cm, (const uint16_t *)Bm, cb};
+    hipLaunchKernelGGL(bmm_chunk_kernel, dim3(s.B * s.nc * s.G), dim3(512), 0, (hipStream_t)stream, a);
+    return launched(hipGetLastError());
+}
+
+ta_status ssd_state_passing(const float *states, const float *dt, const float *A, float *prev_states,
+                            float *final_states, int batch, int seqlen, int nheads, int headdim,
+                            int dstate, int chunk_size, void *stream)
+{
+    if (!states || !dt || !A || !prev_states)
+        return TA_ERR_NULL_POINTER;
+    SsdShape s;
+    const ta_status st = check_shape(batch, seqlen, nheads, 1, headdim, dstate, chunk_size, s);
+    if (st != TA_OK)
+        return st;
+    if (misaligned(states) || misaligned(prev_states) || misaligned(final_states) ||
+        ((uintptr_t)dt & 3) || ((uintptr_t)A & 3))
+        return TA_ERR_MISALIGNED;
+    const size_t ns = (size_t)batch * s.nc * nheads * SP * SN * 4;
+    const size_t nf = (size_t)batch * nheads * SP * SN * 4;
+    const size_t ndt = (size_t)batch * seqlen * nheads * 4;
+    if (overlaps(prev_states, ns, states, ns) || overlaps(prev_states, ns, dt, ndt) ||
+        overlaps(prev_states, ns, A, (size_t)nheads * 4) || overlaps(final_states, nf, states, ns) ||
+        overlaps(final_states, nf, prev_states, ns) || overlaps(final_states, nf, dt, ndt) ||
+        overlaps(final_states, nf, A, (size_t)nheads * 4))
+        return TA_ERR_ALIASING;
+    PassArgs a{s, states, dt, A, prev_states, final_states};
+    hipLaunchKernelGGL(state_passing_kernel, dim3(s.B * s.H * 4), dim3(NT), 0, (hipStream_t)stream, a);
+    return launched(hipGetLastError());
+}
+
+}  // extern "C"

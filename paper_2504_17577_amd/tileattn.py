@@ -59,6 +59,14 @@ def lib():
     L.mla_split_heuristic.argtypes = [i, i, i, i, ctypes.POINTER(i)]
     L.gemm_bf16.restype = i
     L.gemm_bf16.argtypes = [p, p, p, i, i, i, i, p]
+    L.ssd_chunk_state.restype = i
+    L.ssd_chunk_state.argtypes = [p, p, p, p, p] + [i] * 7 + [p]
+    L.ssd_state_passing.restype = i
+    L.ssd_state_passing.argtypes = [p, p, p, p, p] + [i] * 6 + [p]
+    L.ssd_bmm_chunk.restype = i
+    L.ssd_bmm_chunk.argtypes = [p, p, p] + [i] * 5 + [p]
+    L.ssd_chunk_scan.restype = i
+    L.ssd_chunk_scan.argtypes = [p] * 8 + [i] * 7 + [p]
     L.ta_schedule.restype = i
     L.ta_schedule.argtypes = [i, i, i, i, i, ctypes.POINTER(i), ctypes.POINTER(i)]
     L.ta_tile_shape.restype = i
@@ -313,3 +321,123 @@ def gemm_bf16(a, b, out=None, out_dtype=None, stream=None):
     if rc != TA_OK:
         raise TileAttnError(rc, ta_status_string(rc))
     return out
+
+
+# ---------------------------------------------------------------------------
+# Mamba-2 SSD chunk functions (include/tileattn.h documents them in full).
+# Tensors: x [B, L, H, P] bf16; Bm, Cm [B, L, G, N] bf16; dt [B, L, H],
+# A [H], D [H] fp32; cb [B, nc, G, Q, Q], states [B, nc, H, P, N] fp32.
+
+SSD_CHUNK = 256
+
+
+def _ssd_check(name, t, dtype, shape):
+    import torch
+
+    if t.dtype != dtype or not t.is_cuda or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous {dtype} GPU tensor of shape {tuple(shape)}")
+
+
+def _ssd_dims(x, Bm):
+    Bsz, L, H, P = x.shape
+    G, N = Bm.shape[2], Bm.shape[3]
+    return Bsz, L, H, G, P, N, -(-L // SSD_CHUNK)
+
+
+def _ssd_raise(rc):
+    if rc != TA_OK:
+        raise TileAttnError(rc, ta_status_string(rc))
+
+
+def ssd_chunk_state(x, Bm, dt, A, out=None, stream=None):
+    """states [B, nc, H, P, N] fp32 of each chunk started from zero."""
+    import torch
+
+    Bsz, L, H, G, P, N, nc = _ssd_dims(x, Bm)
+    _ssd_check("x", x, torch.bfloat16, (Bsz, L, H, P))
+    _ssd_check("Bm", Bm, torch.bfloat16, (Bsz, L, G, N))
+    _ssd_check("dt", dt, torch.float32, (Bsz, L, H))
+    _ssd_check("A", A, torch.float32, (H,))
+    if out is None:
+        out = torch.empty((Bsz, nc, H, P, N), dtype=torch.float32, device=x.device)
+    _ssd_check("out", out, torch.float32, (Bsz, nc, H, P, N))
+    stream = stream or torch.cuda.current_stream(x.device)
+    _ssd_raise(lib().ssd_chunk_state(x.data_ptr(), Bm.data_ptr(), dt.data_ptr(), A.data_ptr(),
+                                     out.data_ptr(), Bsz, L, H, G, P, N, SSD_CHUNK,
+                                     stream.cuda_stream))
+    return out
+
+
+def ssd_state_passing(states, dt, A, prev=None, final=None, stream=None):
+    """(prev_states [B, nc, H, P, N], final_states [B, H, P, N]): the state
+    each chunk enters with, and the state after the last chunk."""
+    import torch
+
+    Bsz, nc, H, P, N = states.shape
+    L = dt.shape[1]
+    _ssd_check("states", states, torch.float32, (Bsz, nc, H, P, N))
+    _ssd_check("dt", dt, torch.float32, (Bsz, L, H))
+    _ssd_check("A", A, torch.float32, (H,))
+    if -(-L // SSD_CHUNK) != nc:
+        raise TileAttnError(2, "states and dt disagree on the number of chunks")
+    if prev is None:
+        prev = torch.empty_like(states)
+    if final is None:
+        final = torch.empty((Bsz, H, P, N), dtype=torch.float32, device=states.device)
+    _ssd_check("prev", prev, torch.float32, (Bsz, nc, H, P, N))
+    _ssd_check("final", final, torch.float32, (Bsz, H, P, N))
+    stream = stream or torch.cuda.current_stream(states.device)
+    _ssd_raise(lib().ssd_state_passing(states.data_ptr(), dt.data_ptr(), A.data_ptr(),
+                                       prev.data_ptr(), final.data_ptr(), Bsz, L, H, P, N,
+                                       SSD_CHUNK, stream.cuda_stream))
+    return prev, final
+
+
+def ssd_bmm_chunk(Cm, Bm, out=None, stream=None):
+    """cb [B, nc, G, Q, Q] fp32: cb[l][s] = Cm_l . Bm_s inside each chunk."""
+    import torch
+
+    Bsz, L, G, N = Cm.shape
+    nc = -(-L // SSD_CHUNK)
+    _ssd_check("Cm", Cm, torch.bfloat16, (Bsz, L, G, N))
+    _ssd_check("Bm", Bm, torch.bfloat16, (Bsz, L, G, N))
+    if out is None:
+        out = torch.empty((Bsz, nc, G, SSD_CHUNK, SSD_CHUNK), dtype=torch.float32, device=Cm.device)
+    _ssd_check("out", out, torch.float32, (Bsz, nc, G, SSD_CHUNK, SSD_CHUNK))
+    stream = stream or torch.cuda.current_stream(Cm.device)
+    _ssd_raise(lib().ssd_bmm_chunk(Cm.data_ptr(), Bm.data_ptr(), out.data_ptr(), Bsz, L, G, N,
+                                   SSD_CHUNK, stream.cuda_stream))
+    return out
+
+
+def ssd_chunk_scan(x, Cm, cb, dt, A, prev_states, D=None, out=None, stream=None):
+    """y [B, L, H, P] fp32 of the chunk-scan function."""
+    import torch
+
+    Bsz, L, H, G, P, N, nc = _ssd_dims(x, Cm)
+    _ssd_check("x", x, torch.bfloat16, (Bsz, L, H, P))
+    _ssd_check("Cm", Cm, torch.bfloat16, (Bsz, L, G, N))
+    _ssd_check("cb", cb, torch.float32, (Bsz, nc, G, SSD_CHUNK, SSD_CHUNK))
+    _ssd_check("dt", dt, torch.float32, (Bsz, L, H))
+    _ssd_check("A", A, torch.float32, (H,))
+    _ssd_check("prev_states", prev_states, torch.float32, (Bsz, nc, H, P, N))
+    if D is not None:
+        _ssd_check("D", D, torch.float32, (H,))
+    if out is None:
+        out = torch.empty((Bsz, L, H, P), dtype=torch.float32, device=x.device)
+    _ssd_check("out", out, torch.float32, (Bsz, L, H, P))
+    stream = stream or torch.cuda.current_stream(x.device)
+    _ssd_raise(lib().ssd_chunk_scan(x.data_ptr(), Cm.data_ptr(), cb.data_ptr(), dt.data_ptr(),
+                                    A.data_ptr(), prev_states.data_ptr(),
+                                    D.data_ptr() if D is not None else None, out.data_ptr(),
+                                    Bsz, L, H, G, P, N, SSD_CHUNK, stream.cuda_stream))
+    return out
+
+
+def ssd_forward(x, dt, A, Bm, Cm, D=None, stream=None):
+    """The four SSD functions chained on the GPU: (y [B, L, H, P], final
+    states [B, H, P, N])."""
+    states = ssd_chunk_state(x, Bm, dt, A, stream=stream)
+    prev, final = ssd_state_passing(states, dt, A, stream=stream)
+    cb = ssd_bmm_chunk(Cm, Bm, stream=stream)
+    return ssd_chunk_scan(x, Cm, cb, dt, A, prev, D, stream=stream), final

@@ -242,3 +242,59 @@ def test_gemm_validation_before_any_hip_call(change, status):
     a = dict(GEMM_OK, **change)
     rc = ta.gemm_bf16_raw(a["A"], a["B"], a["C"], a["c_bf16"], a["M"], a["N"], a["K"], a["stream"])
     assert rc == status, f"{change}: got {ta.STATUS.get(rc, rc)}, want {ta.STATUS[status]}"
+
+
+# SSD chunk functions: argument errors before any HIP call (fake pointers).
+# Shapes: B=1, L=300, H=4, G=2 -> x 153600 B, Bm/Cm 153600 B, dt 4800 B,
+# cb 2 chunks x 2 groups x 256 KiB, states 2 x 4 x 32 KiB.
+SX, SB, SC, SDT, SA, SD = 0x10000000, 0x11000000, 0x12000000, 0x13000000, 0x14000000, 0x15000000
+SCB, SST, SOUT = 0x20000000, 0x30000000, 0x40000000
+SSD_OK = dict(x=SX, Bm=SB, Cm=SC, cb=SCB, dt=SDT, A=SA, prev=SST, D=SD, out=SOUT, B=1, L=300,
+              H=4, G=2, P=64, N=128, Q=256)
+BAD_SSD = [
+    (dict(x=0), 1), (dict(Cm=0), 1), (dict(cb=0), 1), (dict(dt=0), 1), (dict(A=0), 1),
+    (dict(prev=0), 1), (dict(out=0), 1),
+    (dict(B=0), 2), (dict(L=0), 2), (dict(H=0), 2), (dict(G=0), 2), (dict(H=6, G=4), 2),
+    (dict(P=128), 3), (dict(N=64), 3), (dict(Q=128), 3),
+    (dict(x=SX + 8), 4), (dict(cb=SCB + 4), 4), (dict(out=SOUT + 8), 4), (dict(dt=SDT + 2), 4),
+    (dict(out=SX + 1024), 6), (dict(out=SCB - 4096), 6), (dict(out=SST + 16), 6),
+    (dict(out=SD - 16), 6),
+]
+
+
+@no_gpu
+@pytest.mark.parametrize("change,status", BAD_SSD, ids=[str(c) for c, _ in BAD_SSD])
+def test_ssd_scan_validation_before_any_hip_call(change, status):
+    a = dict(SSD_OK, **change)
+    rc = ta.lib().ssd_chunk_scan(a["x"], a["Cm"], a["cb"], a["dt"], a["A"], a["prev"], a["D"],
+                                 a["out"], a["B"], a["L"], a["H"], a["G"], a["P"], a["N"],
+                                 a["Q"], None)
+    assert rc == status, f"{change}: got {ta.STATUS.get(rc, rc)}, want {ta.STATUS[status]}"
+
+
+BAD_SSD_STATE = [
+    (dict(x=0), 1), (dict(Bm=0), 1), (dict(out=0), 1), (dict(L=-5), 2), (dict(H=3, G=2), 2),
+    (dict(N=256), 3), (dict(Bm=SB + 2), 4), (dict(out=SB + 4096), 6), (dict(out=SDT), 6),
+]
+
+
+@no_gpu
+@pytest.mark.parametrize("change,status", BAD_SSD_STATE, ids=[str(c) for c, _ in BAD_SSD_STATE])
+def test_ssd_state_validation_before_any_hip_call(change, status):
+    a = dict(SSD_OK, **change)
+    rc = ta.lib().ssd_chunk_state(a["x"], a["Bm"], a["dt"], a["A"], a["out"], a["B"], a["L"],
+                                  a["H"], a["G"], a["P"], a["N"], a["Q"], None)
+    assert rc == status, f"{change}: got {ta.STATUS.get(rc, rc)}, want {ta.STATUS[status]}"
+
+
+@no_gpu
+def test_ssd_bmm_and_passing_validation_before_any_hip_call():
+    L = ta.lib()
+    assert L.ssd_bmm_chunk(SC, SB, 0, 1, 300, 2, 128, 256, None) == 1
+    assert L.ssd_bmm_chunk(SC, SB, SCB, 1, 300, 2, 128, 128, None) == 3
+    assert L.ssd_bmm_chunk(SC, SB, SC + 64, 1, 300, 2, 128, 256, None) == 6
+    assert L.ssd_bmm_chunk(SC + 4, SB, SCB, 1, 300, 2, 128, 256, None) == 4
+    assert L.ssd_state_passing(SST, SDT, SA, 0, None, 1, 300, 4, 64, 128, 256, None) == 1
+    assert L.ssd_state_passing(SST, SDT, SA, SOUT, None, 1, 300, 4, 32, 128, 256, None) == 3
+    assert L.ssd_state_passing(SST, SDT, SA, SST + 1024, None, 1, 300, 4, 64, 128, 256, None) == 6
+    assert L.ssd_state_passing(SST, SDT, SA, SOUT, SOUT + 64, 1, 300, 4, 64, 128, 256, None) == 6
