@@ -16,6 +16,9 @@ bounded sample of the same workload as a reported baseline.
   python bench.py --workload mla_b64_s8k [--splits auto|N]
                                     # one multi-head latent attention decode step
                                     # (mla_decode) instead of attn_fwd
+  python bench.py --workload ssd_b64_s8k [--op chunk_scan|chunk_state]
+                                    # one Mamba-2 SSD chunk function at one of the
+                                    # paper's linear-attention shapes
   python bench.py --sustain 8 [--gemm-reference]
                                     # run the step back to back for 8 s while
                                     # sampling board power and XCD clocks
@@ -352,6 +355,119 @@ def bench_gemm(args, torch, tileattn):
     print(json.dumps(result), flush=True)
 
 
+SSD_METRIC = {"chunk_scan": "SSD chunk-scan throughput (algorithmic HBM GB/s), 1 GPU",
+              "chunk_state": "SSD chunk-state throughput (algorithmic HBM GB/s), 1 GPU"}
+
+
+def bench_ssd(args, torch, tileattn):
+    """One Mamba-2 SSD chunk function per step (chunk_scan by default, or
+    chunk_state) at an SSD workload.  Its other inputs (states, the chunk
+    matrix) are made beforehand on the GPU by the library's own chunk-state,
+    state-passing and chunk-matrix kernels."""
+    import oracle.ssd as ossd
+
+    op = args.op or "chunk_scan"
+    w = gen.SSD_WORKLOADS[args.workload]
+    inp = gen.make_ssd_inputs(w, seed=args.seed)
+    f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+    dx, dB, dC = (to_device(inp[k], torch) for k in ("x", "Bm", "Cm"))
+    ddt, dA, dD = f32(inp["dt"]), f32(inp["A"]), f32(inp["D"])
+    stream = torch.cuda.current_stream()
+    states = tileattn.ssd_chunk_state(dx, dB, ddt, dA, stream=stream)
+    prev, _ = tileattn.ssd_state_passing(states, ddt, dA, stream=stream)
+    cb = tileattn.ssd_bmm_chunk(dC, dB, stream=stream)
+    y = torch.empty((w.B, w.L, w.H, w.P), dtype=torch.float32, device="cuda")
+    if op == "chunk_scan":
+        def step():
+            tileattn.ssd_chunk_scan(dx, dC, cb, ddt, dA, prev, dD, out=y, stream=stream)
+        flops, nbytes = w.flops_scan(), w.bytes_scan()
+    else:
+        def step():
+            tileattn.ssd_chunk_state(dx, dB, ddt, dA, out=states, stream=stream)
+        flops, nbytes = w.flops_state(), w.bytes_state()
+    step()
+    torch.cuda.synchronize()
+
+    # spot check two (batch, head) slices against the oracle's own chain
+    Q = w.Q
+    worst = 0.0
+    for b, h in ((0, 0), (w.B - 1, w.H - 1)):
+        g = h // (w.H // w.G)
+        sub = dict(x=inp["x"][b:b + 1, :, [h]], Bm=inp["Bm"][b:b + 1, :, [g]],
+                   Cm=inp["Cm"][b:b + 1, :, [g]], dt=inp["dt"][b:b + 1, :, [h]],
+                   A=inp["A"][[h]], D=inp["D"][[h]])
+        if op == "chunk_scan":
+            ref, _ = ossd.ssd_forward(sub["x"], sub["dt"], sub["A"], sub["Bm"], sub["Cm"], sub["D"], Q)
+            ab = lambda u: np.ascontiguousarray(u) & np.uint16(0x7FFF)
+            s_abs = ossd.chunk_state_abs(sub["x"], sub["Bm"], sub["dt"], sub["A"], Q)
+            p_abs, _ = ossd.state_passing(s_abs, sub["dt"], sub["A"], Q)
+            cb_abs = ossd.bmm_chunk(ab(sub["Cm"]), ab(sub["Bm"]), Q)
+            scale = ossd.chunk_scan_abs(sub["x"], sub["Cm"], cb_abs, sub["dt"], sub["A"], p_abs,
+                                        sub["D"], Q)
+            got, bound = y[b:b + 1, :, [h]].cpu().numpy(), 2.0 ** -6
+        else:
+            ref = ossd.chunk_state(sub["x"], sub["Bm"], sub["dt"], sub["A"], Q)
+            scale = ossd.chunk_state_abs(sub["x"], sub["Bm"], sub["dt"], sub["A"], Q)
+            got, bound = states[b:b + 1, :, [h]].cpu().numpy(), 2.0 ** -7
+        worst = max(worst, float((np.abs(got - ref) / np.maximum(scale, 1e-30)).max() / bound))
+    if not worst <= 1.0:
+        raise SystemExit(f"bench: result check failed (worst err/bound {worst})")
+
+    for _ in range(args.warmup):
+        step()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = start.elapsed_time(end) / args.steps
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    result = {
+        "metric": SSD_METRIC[op], "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "op": op, "shape": w.describe(), "B": w.B, "L": w.L,
+                   "H": w.H, "G": w.G, "P": w.P, "N": w.N, "chunk": w.Q, "seed": args.seed,
+                   "flops_per_step": flops, "bytes_per_step": nbytes},
+        "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None},
+        "wall_s_timed": round(wall, 4),
+        "check": {"worst_err_over_bound": worst, "slices": 2},
+    }
+    if not args.no_cpu_baseline:
+        # the oracle's chain on whole (batch, head) slices, about 10 s
+        def one(b, h):
+            g = h // (w.H // w.G)
+            xs, dts = inp["x"][b:b + 1, :, [h]], inp["dt"][b:b + 1, :, [h]]
+            if op == "chunk_scan":
+                ossd.chunk_scan(xs, inp["Cm"][b:b + 1, :, [g]], np.zeros((1, w.nc, 1, Q, Q)), dts,
+                                inp["A"][[h]], np.zeros((1, w.nc, 1, w.P, w.N)), inp["D"][[h]], Q)
+            else:
+                ossd.chunk_state(xs, inp["Bm"][b:b + 1, :, [g]], dts, inp["A"][[h]], Q)
+        t0 = time.perf_counter()
+        one(0, 0)
+        t1 = max(time.perf_counter() - t0, 1e-6)
+        n = int(max(1, min(w.B * w.H, 10.0 / t1)))
+        t0 = time.perf_counter()
+        for i in range(n):
+            one(i // w.H % w.B, i % w.H)
+        dt_s = time.perf_counter() - t0
+        frac = n / (w.B * w.H)
+        result["cpu_baseline"] = {
+            "value": round(nbytes * frac / dt_s / 1e9, 3), "unit": "GB/s",
+            "cores": len(os.sched_getaffinity(0)), "kind": "oracle",
+            "sample": f"{n} of {w.B * w.H} (batch, head) slices of {w.name}, {op}, numpy float64, "
+                      f"{dt_s:.1f} s wall"}
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -359,7 +475,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
                     choices=sorted(gen.WORKLOADS) + sorted(gen.MLA_WORKLOADS)
-                    + sorted(gen.GEMM_WORKLOADS))
+                    + sorted(gen.GEMM_WORKLOADS) + sorted(gen.SSD_WORKLOADS))
+    ap.add_argument("--op", choices=("chunk_scan", "chunk_state"), default=None,
+                    help="SSD workloads: the function timed (default chunk_scan)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--out", choices=("f32", "bf16"), default=None,
                     help="output dtype: attention O f32 (default, attn_fwd) or bf16 "
@@ -395,6 +513,9 @@ def main():
         return
     if args.workload in gen.GEMM_WORKLOADS:
         bench_gemm(args, torch, tileattn)
+        return
+    if args.workload in gen.SSD_WORKLOADS:
+        bench_ssd(args, torch, tileattn)
         return
     if args.out is None:
         args.out = "f32"

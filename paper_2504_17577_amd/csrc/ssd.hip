@@ -125,6 +125,15 @@ __device__ __forceinline__ bf16x8 tr_operand(const unsigned char *tile, int k0, 
     return __builtin_bit_cast(bf16x8, u32x4{l2[0], l2[1], h2[0], h2[1]});
 }
 
+// Loads of sequence positions past L read the last real position instead
+// (always a valid address) and are zeroed after the load: no branch, so the
+// compiler can issue a whole batch of them before the first wait.
+__device__ __forceinline__ u32x4 load_row16(const uint16_t *p, bool keep)
+{
+    const u32x4 v = *(const u32x4 *)p;
+    return keep ? v : u32x4{0u, 0u, 0u, 0u};
+}
+
 struct SsdShape {
     int B, L, H, G, nc;
     int hpg;   // H / G
@@ -140,12 +149,17 @@ struct StateArgs {
     float *states;
 };
 
-__global__ __launch_bounds__(NT, 2) void chunk_state_kernel(StateArgs args)
+__global__ __launch_bounds__(NT, 6) void chunk_state_kernel(StateArgs args)
 {
+    // Positions are staged in passes of 32 (Bm 8 KB + weighted x 4 KB of LDS,
+    // so many workgroups share a CU and cover each other's memory latency);
+    // the global loads of pass k + 1 are issued into registers before the
+    // MFMAs of pass k.
     const StateArgs &a = args;
-    constexpr int HALF = SQ / 2;   // positions staged per pass
-    __shared__ __attribute__((aligned(16))) unsigned char bt[HALF * SN * 2];   // Bm rows, 32 KB
-    __shared__ __attribute__((aligned(16))) unsigned char xt[HALF * SP * 2];   // weighted x rows, 16 KB
+    constexpr int PASS = 32;
+    constexpr int NPASS = SQ / PASS;
+    __shared__ __attribute__((aligned(16))) unsigned char bt[PASS * SN * 2];
+    __shared__ __attribute__((aligned(16))) unsigned char xt[PASS * SP * 2];
     __shared__ float wts[SQ];
     __shared__ float wsum[4];
     __shared__ float alast;
@@ -158,15 +172,33 @@ __global__ __launch_bounds__(NT, 2) void chunk_state_kernel(StateArgs args)
     const int b = logical / (a.s.H * a.s.nc);
     const int g = h / a.s.hpg;
 
+    // per-thread staging slots of a pass: two 16-byte chunks of Bm (rows of
+    // 16 chunks) and one of x (rows of 8 chunks)
+    const size_t brow = (size_t)a.s.G * SN;          // Bm elements per position
+    const size_t xrow = (size_t)a.s.H * SP;          // x elements per position
+    const int rb0 = tid >> 4, rb1 = (NT + tid) >> 4, cb_ = tid & 15;
+    const int rx = tid >> 3, cx = tid & 7;
+    const uint16_t *bsrc = a.Bm + (size_t)b * a.s.L * brow + (size_t)g * SN + cb_ * 8;
+    const uint16_t *xsrc = a.x + (size_t)b * a.s.L * xrow + (size_t)h * SP + cx * 8;
+    u32x4 nb0, nb1, nx;
+    auto load_pass = [&](int k) {
+        const int p0 = c * SQ + k * PASS;
+        nb0 = *(const u32x4 *)(bsrc + (size_t)min(p0 + rb0, a.s.L - 1) * brow);
+        nb1 = *(const u32x4 *)(bsrc + (size_t)min(p0 + rb1, a.s.L - 1) * brow);
+        nx = *(const u32x4 *)(xsrc + (size_t)min(p0 + rx, a.s.L - 1) * xrow);
+    };
+    load_pass(0);
+
     // cumulative log-decay of this chunk and the per-position weights
     const int t = c * SQ + tid;
-    const float dtl = t < a.s.L ? a.dt[((size_t)b * a.s.L + t) * a.s.H + h] : 0.f;
+    const float dtv = a.dt[((size_t)b * a.s.L + min(t, a.s.L - 1)) * a.s.H + h];
+    const float dtl = t < a.s.L ? dtv : 0.f;
     const float cum = block_scan(dtl * a.A[h], wsum);
     if (tid == NT - 1)
         alast = cum;
     __syncthreads();
     const float a_last = alast;
-    wts[tid] = exp2f((a_last - cum) * LOG2E) * dtl;
+    wts[tid] = exp2f((a_last - cum) * LOG2E) * dtl;   // 0 past L
 
     f32x16 acc[2];
 #pragma unroll
@@ -175,38 +207,26 @@ __global__ __launch_bounds__(NT, 2) void chunk_state_kernel(StateArgs args)
         for (int r = 0; r < 16; ++r)
             acc[pb][r] = 0.f;
 
-    const size_t brow = (size_t)a.s.G * SN;          // Bm elements per position
-    const size_t xrow = (size_t)a.s.H * SP;          // x elements per position
-    for (int half = 0; half < 2; ++half) {
-        __syncthreads();   // wts visible; previous pass's reads done
-        const int p0 = c * SQ + half * HALF;
-        // Bm: 128 rows x 16 chunks of 16 bytes
+    for (int k = 0; k < NPASS; ++k) {
+        __syncthreads();   // wts visible; the previous pass's operand reads done
+        const int p0 = c * SQ + k * PASS;
+        // Bm rows past L are zeroed (they would meet a zero weight anyway,
+        // but the masked product must not see arbitrary bits)
+        *(u32x4 *)(bt + rb0 * (SN * 2) + ((cb_ ^ swz_tr256(rb0)) * 16)) =
+            p0 + rb0 < a.s.L ? nb0 : u32x4{0u, 0u, 0u, 0u};
+        *(u32x4 *)(bt + rb1 * (SN * 2) + ((cb_ ^ swz_tr256(rb1)) * 16)) =
+            p0 + rb1 < a.s.L ? nb1 : u32x4{0u, 0u, 0u, 0u};
+        const float w = wts[k * PASS + rx];
+        u32x4 v;
 #pragma unroll
-        for (int i = 0; i < HALF * 16 / NT; ++i) {
-            const int q = i * NT + tid, r = q >> 4, cc = q & 15;
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (p0 + r < a.s.L)
-                v = *(const u32x4 *)(a.Bm + ((size_t)b * a.s.L + p0 + r) * brow + (size_t)g * SN + cc * 8);
-            *(u32x4 *)(bt + r * (SN * 2) + ((cc ^ swz_tr256(r)) * 16)) = v;
-        }
-        // x: 128 rows x 8 chunks, each scaled by its position's weight
-#pragma unroll
-        for (int i = 0; i < HALF * 8 / NT; ++i) {
-            const int q = i * NT + tid, r = q >> 3, cc = q & 7;
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (p0 + r < a.s.L) {
-                const u32x4 u = *(const u32x4 *)(a.x + ((size_t)b * a.s.L + p0 + r) * xrow +
-                                                 (size_t)h * SP + cc * 8);
-                const float w = wts[half * HALF + r];
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    v[e] = pack_bf16(bf16_lo(u[e]) * w, bf16_hi(u[e]) * w);
-            }
-            *(u32x4 *)(xt + r * (SP * 2) + ((cc ^ swz_tr128(r)) * 16)) = v;
-        }
+        for (int e = 0; e < 4; ++e)
+            v[e] = pack_bf16(bf16_lo(nx[e]) * w, bf16_hi(nx[e]) * w);
+        *(u32x4 *)(xt + rx * (SP * 2) + ((cx ^ swz_tr128(rx)) * 16)) = v;
         __syncthreads();
+        if (k + 1 < NPASS)
+            load_pass(k + 1);
 #pragma unroll
-        for (int ks = 0; ks < HALF / 16; ++ks) {
+        for (int ks = 0; ks < PASS / 16; ++ks) {
             const bf16x8 av = tr_operand<SN * 2, swz_tr256>(bt, 16 * ks, 32 * wave, lane);
 #pragma unroll
             for (int pb = 0; pb < 2; ++pb) {
@@ -241,13 +261,13 @@ struct ScanArgs {
     float *out;
 };
 
-__global__ __launch_bounds__(NT, 2) void chunk_scan_kernel(ScanArgs args)
+__global__ __launch_bounds__(NT, 3) void chunk_scan_kernel(ScanArgs args)
 {
     const ScanArgs &a = args;
     __shared__ __attribute__((aligned(16))) unsigned char xt[SQ * SP * 2];    // x rows, 32 KB
     __shared__ __attribute__((aligned(16))) unsigned char ht[SP * SN * 2];    // Hin (bf16), 16 KB
     __shared__ __attribute__((aligned(16))) float a2s[SQ];                    // log2-domain a_l
-    __shared__ __attribute__((aligned(16))) float g2s[SQ];                    // a2_s - log2(dt_s)
+    __shared__ __attribute__((aligned(16))) float fs[SQ];                     // see below
     __shared__ float wsum[4];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -261,20 +281,38 @@ __global__ __launch_bounds__(NT, 2) void chunk_scan_kernel(ScanArgs args)
 
     const int t = t0 + tid;
     const bool valid = t < a.s.L;
-    const float dtl = valid ? a.dt[((size_t)b * a.s.L + t) * a.s.H + h] : 0.f;
+    const float dtv = a.dt[((size_t)b * a.s.L + min(t, a.s.L - 1)) * a.s.H + h];
+    const float dtl = valid ? dtv : 0.f;
     const float a2 = block_scan(dtl * a.A[h], wsum) * LOG2E;
     a2s[tid] = a2;
-    g2s[tid] = valid ? a2 - log2f(dtl) : INFINITY;   // padded positions weigh zero
 
     // stage x (256 rows x 8 chunks) and the entering state as bf16 (64 rows
     // x 16 chunks, each from 8 fp32)
+    // this wave's 32-position blocks: {wave, 7 - wave} (balances the causal
+    // work); their Cm rows, the B operands of the entering-state term, are
+    // loaded first so they arrive while x and the state are staged.  A
+    // position past L reads row L - 1: it only feeds an output row past L,
+    // which is never stored.
+    const int col = lane & 31, hl = lane >> 5;
+    const int lbs[2] = {wave, 7 - wave};
+    const size_t crow = (size_t)a.s.G * SN;
+    u32x4 cv[2][SN / 16];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int tl = min(t0 + 32 * lbs[i] + col, a.s.L - 1);
+        const uint16_t *cp = a.Cm + ((size_t)b * a.s.L + tl) * crow + (size_t)g * SN + 8 * hl;
+#pragma unroll
+        for (int ks = 0; ks < SN / 16; ++ks)
+            cv[i][ks] = *(const u32x4 *)(cp + 16 * ks);
+    }
+
     const size_t xrow = (size_t)a.s.H * SP;
 #pragma unroll
     for (int i = 0; i < SQ * 8 / NT; ++i) {
         const int q = i * NT + tid, r = q >> 3, cc = q & 7;
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (t0 + r < a.s.L)
-            v = *(const u32x4 *)(a.x + ((size_t)b * a.s.L + t0 + r) * xrow + (size_t)h * SP + cc * 8);
+        const int tr = min(t0 + r, a.s.L - 1);
+        const u32x4 v = load_row16(a.x + ((size_t)b * a.s.L + tr) * xrow + (size_t)h * SP + cc * 8,
+                                   t0 + r < a.s.L);
         *(u32x4 *)(xt + r * (SP * 2) + ((cc ^ swz_tr128(r)) * 16)) = v;
     }
     const float *hin = a.prev + (((size_t)b * a.s.nc + c) * a.s.H + h) * (SP * SN);
@@ -287,11 +325,26 @@ __global__ __launch_bounds__(NT, 2) void chunk_scan_kernel(ScanArgs args)
                          pack_bf16(f1.z, f1.w)};
         *(u32x4 *)(ht + r * (SN * 2) + ((cc ^ swz_row256(r)) * 16)) = v;
     }
+    // the Cm operands are needed from here on: this empty asm uses them, so
+    // the compiler issues their loads above (with the staging loads) instead
+    // of one k-step at a time after the barrier
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int ks = 0; ks < SN / 16; ++ks)
+            asm volatile("" : "+v"(cv[i][ks]));
+    __syncthreads();
+    // The within-chunk weight exp(a_l - a_s) dt_s is split at the last
+    // position e(s) of the 16-position block holding s:
+    //   fs[s] = dt_s exp(a_e(s) - a_s)  (<= dt_s, formed once per position)
+    //   r_l   = exp(a_l - a_e(s))       (one per lane and 16-position step)
+    // so a weight costs two multiplies instead of an exponential.  Both
+    // factors are finite for every (l, s) of a step: a_e - a_s spans at most
+    // 16 positions; r_l > 1 only on steps crossing the diagonal, where the
+    // products with s > l are masked to zero.
+    fs[tid] = valid ? dtl * __builtin_amdgcn_exp2f(a2s[(tid | 15)] - a2) : 0.f;
     __syncthreads();
 
-    const int col = lane & 31, hl = lane >> 5;
-    // this wave's 32-position blocks: {wave, 7 - wave} (balances the causal work)
-    const int lbs[2] = {wave, 7 - wave};
     f32x16 acc[2][2];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -302,29 +355,19 @@ __global__ __launch_bounds__(NT, 2) void chunk_scan_kernel(ScanArgs args)
                 acc[i][pb][r] = 0.f;
 
     // entering state: A = Hin rows (p), B = Cm rows (l), k = n
-    const size_t crow = (size_t)a.s.G * SN;
 #pragma unroll
     for (int ks = 0; ks < SN / 16; ++ks) {
-        bf16x8 av[2], bv[2];
+        bf16x8 av[2];
 #pragma unroll
         for (int pb = 0; pb < 2; ++pb) {
             const int r = 32 * pb + col;
             av[pb] = *(const bf16x8 *)(ht + r * (SN * 2) + (((2 * ks + hl) ^ swz_row256(r)) * 16));
         }
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int tl = t0 + 32 * lbs[i] + col;
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (tl < a.s.L)
-                v = *(const u32x4 *)(a.Cm + ((size_t)b * a.s.L + tl) * crow + (size_t)g * SN +
-                                     16 * ks + 8 * hl);
-            bv[i] = __builtin_bit_cast(bf16x8, v);
-        }
-#pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
             for (int pb = 0; pb < 2; ++pb)
-                acc[i][pb] = mfma32(av[pb], bv[i], acc[i][pb]);
+                acc[i][pb] = mfma32(av[pb], __builtin_bit_cast(bf16x8, cv[i][ks]), acc[i][pb]);
     }
     // decay the entering state to each position (lane's column l)
 #pragma unroll
@@ -338,51 +381,71 @@ __global__ __launch_bounds__(NT, 2) void chunk_scan_kernel(ScanArgs args)
     }
 
     // within the chunk: A = x^T (p, s) by transpose reads, B = the weighted
-    // cb row of position l, k = s <= l
+    // cb row of position l, k = s <= l.  Each k-step needs 8 values of the
+    // lane's cb row, cbr[16k .. 16k+3] and cbr[16k+8 .. 16k+11]; four
+    // register sets rotate, each reloaded four k-steps ahead right after it
+    // is consumed.  The step count of a block is rounded up to a multiple of
+    // four: the extra steps lie above the diagonal (every weight masked to
+    // zero) and their loads are clamped inside the row.
     const float *cbm = a.cb + (((size_t)b * a.s.nc + c) * a.s.G + g) * (SQ * SQ);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         const int lb = lbs[i];
         const int l = 32 * lb + col;
         const float a2l = a2s[l];
-        const float *cbr = cbm + (size_t)l * SQ;
-        for (int ks = 0; ks <= 2 * lb + 1; ++ks) {
-            const int s_lo = 16 * ks + 4 * hl, s_hi = s_lo + 8;
-            const float4 c0 = *(const float4 *)(cbr + s_lo);
-            const float4 c1 = *(const float4 *)(cbr + s_hi);
-            const float4 q0 = *(const float4 *)(g2s + s_lo);
-            const float4 q1 = *(const float4 *)(g2s + s_hi);
-            float m[8] = {c0.x * exp2f(a2l - q0.x), c0.y * exp2f(a2l - q0.y),
-                          c0.z * exp2f(a2l - q0.z), c0.w * exp2f(a2l - q0.w),
-                          c1.x * exp2f(a2l - q1.x), c1.y * exp2f(a2l - q1.y),
-                          c1.z * exp2f(a2l - q1.z), c1.w * exp2f(a2l - q1.w)};
-            if (ks >= 2 * lb) {   // blocks crossing the diagonal: keep s <= l
+        const float *cbr = cbm + (size_t)l * SQ + 4 * hl;
+        const int n_ks = 2 * lb + 2;
+        const int n_pad = (n_ks + 3) & ~3;
+        const int k_max = 15;   // last k-step inside the row
+        float4 r[4][2];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    m[e] = s_lo + e <= l ? m[e] : 0.f;
-                    m[4 + e] = s_hi + e <= l ? m[4 + e] : 0.f;
+        for (int j = 0; j < 4; ++j) {
+            r[j][0] = *(const float4 *)(cbr + 16 * j);
+            r[j][1] = *(const float4 *)(cbr + 16 * j + 8);
+        }
+        for (int k0 = 0; k0 < n_pad; k0 += 4) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int ks = k0 + j;
+                const float4 c0 = r[j][0], c1 = r[j][1];
+                const int kn = min(ks + 4, k_max);
+                r[j][0] = *(const float4 *)(cbr + 16 * kn);
+                r[j][1] = *(const float4 *)(cbr + 16 * kn + 8);
+                const int s_lo = 16 * ks + 4 * hl, s_hi = s_lo + 8;
+                const float4 q0 = *(const float4 *)(fs + s_lo);
+                const float4 q1 = *(const float4 *)(fs + s_hi);
+                const float rl = __builtin_amdgcn_exp2f(a2l - a2s[16 * ks + 15]);
+                const float cs[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+                const float qs[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
+                float m[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    m[e] = cs[e] * qs[e] * rl;
+                if (ks >= n_ks - 2) {   // the two steps crossing the diagonal: keep s <= l
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int s_e = (e < 4 ? s_lo : s_hi - 4) + e;
+                        m[e] = s_e <= l ? m[e] : 0.f;
+                    }
                 }
-            }
-            const bf16x8 bv = __builtin_bit_cast(
-                bf16x8, u32x4{pack_bf16(m[0], m[1]), pack_bf16(m[2], m[3]), pack_bf16(m[4], m[5]),
-                              pack_bf16(m[6], m[7])});
+                const bf16x8 bv = __builtin_bit_cast(
+                    bf16x8, u32x4{pack_bf16(m[0], m[1]), pack_bf16(m[2], m[3]),
+                                  pack_bf16(m[4], m[5]), pack_bf16(m[6], m[7])});
 #pragma unroll
-            for (int pb = 0; pb < 2; ++pb) {
-                const bf16x8 av = tr_operand<SP * 2, swz_tr128>(xt, 16 * ks, 32 * pb, lane);
-                acc[i][pb] = mfma32(av, bv, acc[i][pb]);
+                for (int pb = 0; pb < 2; ++pb) {
+                    const bf16x8 av = tr_operand<SP * 2, swz_tr128>(xt, 16 * ks, 32 * pb, lane);
+                    acc[i][pb] = mfma32(av, bv, acc[i][pb]);
+                }
             }
         }
     }
 
-    // skip term and store: lane holds y^T[p][l] for l = 32 lb + col and
-    // p = 32 pb + 8 j + 4 hl + 0..3 (four consecutive p of output row l)
+    // skip term: lane holds y^T[p][l] for l = 32 lb + col and p = 32 pb +
+    // 8 j + 4 hl + 0..3 (four consecutive p of output row l)
     const float dh = a.D ? a.D[h] : 0.f;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         const int l = 32 * lbs[i] + col;
-        if (t0 + l >= a.s.L)
-            continue;
-        float *yo = a.out + ((size_t)b * a.s.L + t0 + l) * xrow + (size_t)h * SP;
 #pragma unroll
         for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
@@ -390,11 +453,39 @@ __global__ __launch_bounds__(NT, 2) void chunk_scan_kernel(ScanArgs args)
                 const int p = 32 * pb + 8 * j + 4 * hl;
                 const u32x2 xv = *(const u32x2 *)(xt + l * (SP * 2) + (((p >> 3) ^ swz_tr128(l)) * 16) +
                                                   (2 * p & 15));
-                *(float4 *)(yo + p) = float4{acc[i][pb][4 * j] + dh * bf16_lo(xv[0]),
-                                             acc[i][pb][4 * j + 1] + dh * bf16_hi(xv[0]),
-                                             acc[i][pb][4 * j + 2] + dh * bf16_lo(xv[1]),
-                                             acc[i][pb][4 * j + 3] + dh * bf16_hi(xv[1])};
+                acc[i][pb][4 * j] += dh * bf16_lo(xv[0]);
+                acc[i][pb][4 * j + 1] += dh * bf16_hi(xv[0]);
+                acc[i][pb][4 * j + 2] += dh * bf16_lo(xv[1]);
+                acc[i][pb][4 * j + 3] += dh * bf16_hi(xv[1]);
             }
+    }
+    // Store through LDS so that every global store writes whole rows: each
+    // wave stages one 32 x 64 fp32 block at a time in its 8 KB of the x
+    // tile (16-byte chunk q of row r at q ^ (r & 15), conflict free both
+    // ways), then writes 4 rows of 256 bytes per instruction.  LDS accesses
+    // of one wave complete in order, so the wave needs no barrier of its own.
+    __syncthreads();   // every wave is done with the x tile
+    float *stg = (float *)(xt + wave * (32 * SP * 4));
+    const size_t xrow_ = (size_t)a.s.H * SP;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int q = 8 * pb + 2 * j + hl;
+                *(float4 *)(stg + col * SP + ((q ^ (col & 15)) * 4)) =
+                    float4{acc[i][pb][4 * j], acc[i][pb][4 * j + 1], acc[i][pb][4 * j + 2],
+                           acc[i][pb][4 * j + 3]};
+            }
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+            const int r = 4 * it + (lane >> 4), q = lane & 15;
+            const float4 v = *(const float4 *)(stg + r * SP + ((q ^ (r & 15)) * 4));
+            const int tt = t0 + 32 * lbs[i] + r;
+            if (tt < a.s.L)
+                *(float4 *)(a.out + ((size_t)b * a.s.L + tt) * xrow_ + (size_t)h * SP + 4 * q) = v;
+        }
     }
 }
 
@@ -428,17 +519,16 @@ __global__ __launch_bounds__(512, 1) void bmm_chunk_kernel(BmmArgs args)
     const int ts = t0 + 32 * wave + col;
 #pragma unroll 2
     for (int ks = 0; ks < SN / 16; ++ks) {
-        u32x4 va = {0u, 0u, 0u, 0u};
-        if (ts < a.s.L)
-            va = *(const u32x4 *)(a.Bm + ((size_t)b * a.s.L + ts) * row + (size_t)g * SN + 16 * ks + 8 * hl);
+        const u32x4 va = load_row16(a.Bm + ((size_t)b * a.s.L + min(ts, a.s.L - 1)) * row +
+                                        (size_t)g * SN + 16 * ks + 8 * hl,
+                                    ts < a.s.L);
         const bf16x8 av = __builtin_bit_cast(bf16x8, va);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int tl = t0 + 32 * j + col;
-            u32x4 vb = {0u, 0u, 0u, 0u};
-            if (tl < a.s.L)
-                vb = *(const u32x4 *)(a.Cm + ((size_t)b * a.s.L + tl) * row + (size_t)g * SN + 16 * ks +
-                                      8 * hl);
+            const u32x4 vb = load_row16(a.Cm + ((size_t)b * a.s.L + min(tl, a.s.L - 1)) * row +
+                                            (size_t)g * SN + 16 * ks + 8 * hl,
+                                        tl < a.s.L);
             acc[j] = mfma32(av, __builtin_bit_cast(bf16x8, vb), acc[j]);
         }
     }
@@ -476,7 +566,8 @@ __global__ __launch_bounds__(NT, 4) void state_passing_kernel(PassArgs args)
     float4 h0 = {0.f, 0.f, 0.f, 0.f}, h1 = {0.f, 0.f, 0.f, 0.f};
     for (int c = 0; c < a.s.nc; ++c) {
         const int t = c * SQ + tid;
-        float v = t < a.s.L ? a.dt[((size_t)b * a.s.L + t) * a.s.H + h] : 0.f;
+        const float dtv = a.dt[((size_t)b * a.s.L + min(t, a.s.L - 1)) * a.s.H + h];
+        float v = t < a.s.L ? dtv : 0.f;
 #pragma unroll
         for (int d = 32; d >= 1; d >>= 1)
             v += __shfl_xor(v, d, 64);

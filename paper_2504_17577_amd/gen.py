@@ -298,7 +298,9 @@ def random_gemm_problem(M: int, N: int, K: int, seed: int, wid: int = 102):
 #   D      [H]           fp32     skip weights
 # Recipe: x, Bm, Cm i.i.d. N(0,1); dt = exp(U(ln 1e-3, ln 1e-1)) and
 # A = -exp(U(ln 1, ln 16)), the ranges Mamba-2 initialises them in;
-# D ~ U(0.5, 1.5).  The chunk-scan function also takes the per-chunk matrix
+# D ~ U(0.5, 1.5).  x, Bm and Cm are drawn in blocks of 2^23 elements, one
+# jumped substream per block, by a thread pool (the largest x is 2^31
+# elements).  The chunk-scan function also takes the per-chunk matrix
 # cb [B, nc, G, Q, Q] and the entering states [B, nc, H, P, N] (fp32); for
 # tests of that function alone they are drawn here too: cb ~ N(0, N) (the
 # spread of a dot product of two N-vectors of unit normals), states ~ N(0, 1).
@@ -370,6 +372,31 @@ SSD_WORKLOADS = {
 }
 
 
+BLOCK = 1 << 23   # elements per independently drawn block of a large tensor
+
+
+def normal_bf16_blocks(shape, seed: int, wid: int, tensor: int, threads: int = 16) -> np.ndarray:
+    """i.i.d. N(0,1) samples as bfloat16 bits, drawn in blocks of BLOCK
+    elements: block i comes from the tensor's Philox substream jumped i times
+    (2^128 draws apart), so the result does not depend on ``threads``, and
+    the blocks are drawn by a thread pool (numpy releases the GIL while it
+    fills them)."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    n = int(np.prod(shape))
+    out = np.empty(n, dtype=np.uint16)
+    key = np.array([seed & 0xFFFFFFFFFFFFFFFF, (wid << 8) | tensor], dtype=np.uint64)
+
+    def fill(i):
+        g = np.random.Generator(np.random.Philox(key=key).jumped(i))
+        m = min(BLOCK, n - i * BLOCK)
+        out[i * BLOCK:i * BLOCK + m] = bf16_from_f32(g.standard_normal(size=m, dtype=np.float32))
+
+    with ThreadPoolExecutor(max(1, threads)) as ex:
+        list(ex.map(fill, range(-(-n // BLOCK))))
+    return out.reshape(shape)
+
+
 def _uniform_f32(shape, lo, hi, seed, wid, tensor):
     g = _stream(seed, wid, tensor)
     return g.uniform(lo, hi, size=int(np.prod(shape))).astype(np.float32).reshape(shape)
@@ -379,9 +406,9 @@ def make_ssd_inputs(w: SsdWorkload, seed: int = 0):
     """dict of x, Bm, Cm (bfloat16 bits), dt, A, D (float32) for workload ``w``."""
     ln = math.log
     return {
-        "x": normal_bf16((w.B, w.L, w.H, w.P), seed, w.wid, TENSOR_X),
-        "Bm": normal_bf16((w.B, w.L, w.G, w.N), seed, w.wid, TENSOR_BM),
-        "Cm": normal_bf16((w.B, w.L, w.G, w.N), seed, w.wid, TENSOR_CM),
+        "x": normal_bf16_blocks((w.B, w.L, w.H, w.P), seed, w.wid, TENSOR_X),
+        "Bm": normal_bf16_blocks((w.B, w.L, w.G, w.N), seed, w.wid, TENSOR_BM),
+        "Cm": normal_bf16_blocks((w.B, w.L, w.G, w.N), seed, w.wid, TENSOR_CM),
         "dt": np.exp(_uniform_f32((w.B, w.L, w.H), ln(1e-3), ln(1e-1), seed, w.wid, TENSOR_DT)),
         "A": -np.exp(_uniform_f32((w.H,), ln(1.0), ln(16.0), seed, w.wid, TENSOR_A)),
         "D": _uniform_f32((w.H,), 0.5, 1.5, seed, w.wid, TENSOR_D),
