@@ -288,23 +288,9 @@ __global__ __launch_bounds__(NT, 3) void chunk_scan_kernel(ScanArgs args)
 
     // stage x (256 rows x 8 chunks) and the entering state as bf16 (64 rows
     // x 16 chunks, each from 8 fp32)
-    // this wave's 32-position blocks: {wave, 7 - wave} (balances the causal
-    // work); their Cm rows, the B operands of the entering-state term, are
-    // loaded first so they arrive while x and the state are staged.  A
-    // position past L reads row L - 1: it only feeds an output row past L,
-    // which is never stored.
+    // this wave's 32-position blocks: {wave, 7 - wave} (balances the causal work)
     const int col = lane & 31, hl = lane >> 5;
     const int lbs[2] = {wave, 7 - wave};
-    const size_t crow = (size_t)a.s.G * SN;
-    u32x4 cv[2][SN / 16];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int tl = min(t0 + 32 * lbs[i] + col, a.s.L - 1);
-        const uint16_t *cp = a.Cm + ((size_t)b * a.s.L + tl) * crow + (size_t)g * SN + 8 * hl;
-#pragma unroll
-        for (int ks = 0; ks < SN / 16; ++ks)
-            cv[i][ks] = *(const u32x4 *)(cp + 16 * ks);
-    }
 
     const size_t xrow = (size_t)a.s.H * SP;
 #pragma unroll
@@ -325,14 +311,6 @@ __global__ __launch_bounds__(NT, 3) void chunk_scan_kernel(ScanArgs args)
                          pack_bf16(f1.z, f1.w)};
         *(u32x4 *)(ht + r * (SN * 2) + ((cc ^ swz_row256(r)) * 16)) = v;
     }
-    // the Cm operands are needed from here on: this empty asm uses them, so
-    // the compiler issues their loads above (with the staging loads) instead
-    // of one k-step at a time after the barrier
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int ks = 0; ks < SN / 16; ++ks)
-            asm volatile("" : "+v"(cv[i][ks]));
     __syncthreads();
     // The within-chunk weight exp(a_l - a_s) dt_s is split at the last
     // position e(s) of the 16-position block holding s:
@@ -354,7 +332,15 @@ __global__ __launch_bounds__(NT, 3) void chunk_scan_kernel(ScanArgs args)
             for (int r = 0; r < 16; ++r)
                 acc[i][pb][r] = 0.f;
 
-    // entering state: A = Hin rows (p), B = Cm rows (l), k = n
+    // entering state: A = Hin rows (p), B = Cm rows (l), k = n.  A position
+    // past L reads row L - 1: it only feeds an output row past L, which is
+    // never stored.
+    const size_t crow = (size_t)a.s.G * SN;
+    const uint16_t *cp[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+        cp[i] = a.Cm + ((size_t)b * a.s.L + min(t0 + 32 * lbs[i] + col, a.s.L - 1)) * crow +
+                (size_t)g * SN + 8 * hl;
 #pragma unroll
     for (int ks = 0; ks < SN / 16; ++ks) {
         bf16x8 av[2];
@@ -367,7 +353,8 @@ __global__ __launch_bounds__(NT, 3) void chunk_scan_kernel(ScanArgs args)
         for (int i = 0; i < 2; ++i)
 #pragma unroll
             for (int pb = 0; pb < 2; ++pb)
-                acc[i][pb] = mfma32(av[pb], __builtin_bit_cast(bf16x8, cv[i][ks]), acc[i][pb]);
+                acc[i][pb] = mfma32(av[pb], __builtin_bit_cast(bf16x8, *(const u32x4 *)(cp[i] + 16 * ks)),
+                                    acc[i][pb]);
     }
     // decay the entering state to each position (lane's column l)
 #pragma unroll
@@ -380,64 +367,76 @@ __global__ __launch_bounds__(NT, 3) void chunk_scan_kernel(ScanArgs args)
                 acc[i][pb][r] *= e;
     }
 
-    // within the chunk: A = x^T (p, s) by transpose reads, B = the weighted
-    // cb row of position l, k = s <= l.  Each k-step needs 8 values of the
-    // lane's cb row, cbr[16k .. 16k+3] and cbr[16k+8 .. 16k+11]; four
-    // register sets rotate, each reloaded four k-steps ahead right after it
-    // is consumed.  The step count of a block is rounded up to a multiple of
-    // four: the extra steps lie above the diagonal (every weight masked to
-    // zero) and their loads are clamped inside the row.
+    // within the chunk: A = x^T (p, s) by transpose reads, B = the weight
+    // matrix M[l][s] = cb[l][s] exp(a_l - a_s) dt_s (s <= l).  M is built in
+    // slabs of 32 positions s: all threads read the slab's cb rows (l >=
+    // the slab start) with coalesced 16-byte loads, form the bf16 weights
+    // and write them to an LDS tile (the entering state's space, free after
+    // the first term); the waves then run the slab's two k-steps for their
+    // own position blocks.  The cb loads of slab k + 1 are in flight during
+    // the MFMAs of slab k.
+    //   Weight of (l, s): cb[l][s] fs[s] r, with fs[s] = dt_s exp(a_e - a_s)
+    // and r = exp(a_l - a_e) for e the last position of the 16-block of s
+    // (one exponential per 4 weights; both factors finite, s > l masked).
+    //   M tile: row l, 8-byte unit u (4 weights) at u ^ ((l >> 2) & 7), which
+    // keeps both the staging writes and the operand reads conflict free.
+    __syncthreads();   // every wave is done with the entering state
+    unsigned char *mt = ht;
     const float *cbm = a.cb + (((size_t)b * a.s.nc + c) * a.s.G + g) * (SQ * SQ);
+    const int ld_q = tid & 7;                  // 16-byte quad of the slab row
+    float4 cr[8];                              // this thread's loads of one slab
+    auto load_slab = [&](int k) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int lb = lbs[i];
-        const int l = 32 * lb + col;
-        const float a2l = a2s[l];
-        const float *cbr = cbm + (size_t)l * SQ + 4 * hl;
-        const int n_ks = 2 * lb + 2;
-        const int n_pad = (n_ks + 3) & ~3;
-        const int k_max = 15;   // last k-step inside the row
-        float4 r[4][2];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            r[j][0] = *(const float4 *)(cbr + 16 * j);
-            r[j][1] = *(const float4 *)(cbr + 16 * j + 8);
+        for (int i = 0; i < 8; ++i) {
+            const int row = 32 * k + (i * NT + tid) / 8;   // rows past 255 are not used
+            if (i < 8 - k)
+                cr[i] = *(const float4 *)(cbm + (size_t)row * SQ + 32 * k + 4 * ld_q);
         }
-        for (int k0 = 0; k0 < n_pad; k0 += 4) {
+    };
+    load_slab(0);
+    for (int k = 0; k < SQ / 32; ++k) {
+        // weights of slab k into the tile
+        const int s0 = 32 * k + 4 * ld_q;
+        const float4 fq = *(const float4 *)(fs + s0);
+        const float a2e = a2s[(s0 | 15)];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int ks = k0 + j;
-                const float4 c0 = r[j][0], c1 = r[j][1];
-                const int kn = min(ks + 4, k_max);
-                r[j][0] = *(const float4 *)(cbr + 16 * kn);
-                r[j][1] = *(const float4 *)(cbr + 16 * kn + 8);
-                const int s_lo = 16 * ks + 4 * hl, s_hi = s_lo + 8;
-                const float4 q0 = *(const float4 *)(fs + s_lo);
-                const float4 q1 = *(const float4 *)(fs + s_hi);
-                const float rl = __builtin_amdgcn_exp2f(a2l - a2s[16 * ks + 15]);
-                const float cs[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
-                const float qs[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
-                float m[8];
+        for (int i = 0; i < 8; ++i) {
+            if (i < 8 - k) {
+                const int row = 32 * k + (i * NT + tid) / 8;
+                const float r = __builtin_amdgcn_exp2f(a2s[row] - a2e);
+                const float4 cv4 = cr[i];
+                const float w0 = s0 <= row ? cv4.x * fq.x * r : 0.f;
+                const float w1 = s0 + 1 <= row ? cv4.y * fq.y * r : 0.f;
+                const float w2 = s0 + 2 <= row ? cv4.z * fq.z * r : 0.f;
+                const float w3 = s0 + 3 <= row ? cv4.w * fq.w * r : 0.f;
+                *(u32x2 *)(mt + row * 64 + ((ld_q ^ ((row >> 2) & 7)) * 8)) =
+                    u32x2{pack_bf16(w0, w1), pack_bf16(w2, w3)};
+            }
+        }
+        __syncthreads();
+        if (k + 1 < SQ / 32)
+            load_slab(k + 1);
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    m[e] = cs[e] * qs[e] * rl;
-                if (ks >= n_ks - 2) {   // the two steps crossing the diagonal: keep s <= l
+        for (int i = 0; i < 2; ++i) {
+            const int lb = lbs[i];
+            if (lb < k)
+                continue;
+            const int l = 32 * lb + col;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int s_e = (e < 4 ? s_lo : s_hi - 4) + e;
-                        m[e] = s_e <= l ? m[e] : 0.f;
-                    }
-                }
-                const bf16x8 bv = __builtin_bit_cast(
-                    bf16x8, u32x4{pack_bf16(m[0], m[1]), pack_bf16(m[2], m[3]),
-                                  pack_bf16(m[4], m[5]), pack_bf16(m[6], m[7])});
+            for (int kk = 0; kk < 2; ++kk) {
+                const int u0 = 4 * kk + hl, u1 = u0 + 2;
+                const u32x2 m0 = *(const u32x2 *)(mt + l * 64 + ((u0 ^ ((l >> 2) & 7)) * 8));
+                const u32x2 m1 = *(const u32x2 *)(mt + l * 64 + ((u1 ^ ((l >> 2) & 7)) * 8));
+                const bf16x8 bv = __builtin_bit_cast(bf16x8, u32x4{m0[0], m0[1], m1[0], m1[1]});
 #pragma unroll
                 for (int pb = 0; pb < 2; ++pb) {
-                    const bf16x8 av = tr_operand<SP * 2, swz_tr128>(xt, 16 * ks, 32 * pb, lane);
+                    const bf16x8 av =
+                        tr_operand<SP * 2, swz_tr128>(xt, 32 * k + 16 * kk, 32 * pb, lane);
                     acc[i][pb] = mfma32(av, bv, acc[i][pb]);
                 }
             }
         }
+        __syncthreads();   // the tile is rewritten by the next slab
     }
 
     // skip term: lane holds y^T[p][l] for l = 32 lb + col and p = 32 pb +
