@@ -9,8 +9,10 @@
 //    waves form a 2 x 4 grid, each owning (BM/2) x (BN/4) as 32 x 32 blocks
 //    of v_mfma_f32_32x32x16_bf16 accumulators (fp32).  Two waves share each
 //    SIMD, so one's matrix-core work covers the other's LDS reads and
-//    barrier waits (measured 13-16 % faster than four waves holding twice
-//    the accumulator each).
+//    barrier waits.  Four waves of 128 x 128 each read a third less from LDS
+//    per flop and run at a ~6 % higher clock under the board's power limit,
+//    but with one wave per SIMD their matrix cores idle at every barrier and
+//    operand wait: measured 1-3 % slower at 8192^3 and 4096 x 8192 x 8192.
 //  * K advances in steps of 64.  The A tile [BM][64] and the B tile [64][BN]
 //    go global -> LDS by DMA (buffer_load_dwordx4 ... lds, issued as inline
 //    assembly and waited for explicitly), double-buffered: the DMA of step
