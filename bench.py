@@ -13,6 +13,9 @@ bounded sample of the same workload as a reported baseline.
   python bench.py --workload gemm_m5 [--out f32|bf16]
                                     # C = A B (gemm_bf16) at one of the paper's
                                     # M0-M7 shapes, with hipBLASLt timed beside it
+  python bench.py --workload gemv_v0 [--out f32|bf16]
+                                    # the same call at M = 1 (the paper's V0-V7
+                                    # matrix-vector shapes), HBM-bound
   python bench.py --workload mla_b64_s8k [--splits auto|N]
                                     # one multi-head latent attention decode step
                                     # (mla_decode) instead of attn_fwd
@@ -274,6 +277,7 @@ def bench_mla(args, torch, tileattn):
 
 
 GEMM_METRIC = "GEMM TFLOP/s and % of MI355X bf16 MFMA peak, 1 GPU"
+GEMV_METRIC = "matrix-vector product throughput (algorithmic HBM GB/s), 1 GPU"
 
 
 def bench_gemm(args, torch, tileattn):
@@ -307,10 +311,21 @@ def bench_gemm(args, torch, tileattn):
         return start.elapsed_time(end) / args.steps, time.perf_counter() - t0
 
     ms, wall = timed(step)
-    rows = [0, w.M // 2, w.M - 1]
-    ref = oracle.gemm(a, b, rows=rows)
-    scale = oracle.gemm_abs(a, b, rows=rows)
-    got = c.float()[torch.tensor(rows)].cpu().numpy()
+    gemv = w.M == 1
+    if gemv:
+        # M = 1: sampled columns (the oracle would widen all of B otherwise)
+        rng = np.random.default_rng(args.seed + 1)
+        cols = np.unique(np.concatenate([[0, 63, 64, w.N - 1], rng.integers(0, w.N, size=60)]))
+        bs = np.ascontiguousarray(b[:, cols])
+        ref, scale = oracle.gemm(a, bs)[0], oracle.gemm_abs(a, bs)[0]
+        got = c.float()[0, torch.from_numpy(cols).cuda()].cpu().numpy()
+        checked = {"columns": int(len(cols))}
+    else:
+        rows = [0, w.M // 2, w.M - 1]
+        ref = oracle.gemm(a, b, rows=rows)
+        scale = oracle.gemm_abs(a, b, rows=rows)
+        got = c.float()[torch.tensor(rows)].cpu().numpy()
+        checked = {"rows": len(rows)}
     tol = 1e-5 * scale + (2.0 ** -8 * np.abs(ref) if c_bf16 else 0.0)
     worst = float((np.abs(got - ref) / tol).max())
     if not worst <= 1.0:
@@ -318,40 +333,64 @@ def bench_gemm(args, torch, tileattn):
     ref_out = torch.empty((w.M, w.N), dtype=torch.bfloat16, device="cuda")
     ms_ref, _ = timed(lambda: torch.matmul(da, db, out=ref_out))
     tflops = w.flops() / (ms * 1e-3) / 1e12
-    result = {
-        "metric": GEMM_METRIC, "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+    gbs = w.bytes(2 if c_bf16 else 4) / (ms * 1e-3) / 1e9
+    common = {
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "out_dtype": "bf16" if c_bf16 else "f32", "data": "synthetic",
         "config": {"workload": w.name, "shape": w.describe(), "M": w.M, "N": w.N, "K": w.K,
-                   "seed": args.seed, "flops_per_step": w.flops()},
-        "pct_of_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
-        "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None,
-                     "hbm_gbs_algorithmic": round(w.bytes(2 if c_bf16 else 4) / (ms * 1e-3) / 1e9, 1)},
+                   "seed": args.seed, "flops_per_step": w.flops(),
+                   "bytes_per_step": w.bytes(2 if c_bf16 else 4)},
+    }
+    if gemv:
+        result = {"metric": GEMV_METRIC, "value": round(gbs, 1), "unit": "GB/s", **common,
+                  "pct_of_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+                  "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                               "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                               "traffic": None, "tflops": round(tflops, 3)}}
+    else:
+        result = {"metric": GEMM_METRIC, "value": round(tflops, 2), "unit": "TFLOP/s", **common,
+                  "pct_of_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+                  "roofline": {"bound": "mfma", "achieved": round(tflops, 2),
+                               "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                               "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                               "hbm_gbs_algorithmic": round(gbs, 1)}}
+    result.update({
         "vendor_reference": {"op": "torch.matmul bf16 -> bf16 (hipBLASLt)",
-                             "tflops": round(w.flops() / (ms_ref * 1e-3) / 1e12, 2),
+                             "tflops": round(w.flops() / (ms_ref * 1e-3) / 1e12, 3),
                              "ms_per_call": round(ms_ref, 5),
                              "ratio": round(ms_ref / ms, 4)},
         "wall_s_timed": round(wall, 4),
-        "check": {"worst_err_over_tol": worst, "rows": len(rows)},
-    }
+        "check": {"worst_err_over_tol": worst, **checked},
+    })
     if not args.no_cpu_baseline:
-        # fp64 oracle on a bounded number of rows (about 10 s), calibrated on
-        # 16 rows after one untimed call (the first call pays numpy's set-up)
-        oracle.gemm(a, b, rows=[0])
+        # fp64 oracle on a bounded share of the output (about 10 s), calibrated
+        # on a small share after one untimed call (the first pays numpy's set-up)
+        if gemv:
+            def part(n):
+                return oracle.gemm(a, np.ascontiguousarray(b[:, :n]))
+            total, unit_name, cal = w.N, "columns", 64
+        else:
+            def part(n):
+                return oracle.gemm(a, b, rows=list(range(n)))
+            total, unit_name, cal = w.M, "rows", 16
+        part(1)
         t0 = time.perf_counter()
-        oracle.gemm(a, b, rows=list(range(16)))
-        t1 = max(time.perf_counter() - t0, 1e-6) / 16
-        n = int(max(1, min(w.M, 10.0 / t1)))
+        part(cal)
+        t1 = max(time.perf_counter() - t0, 1e-6) / cal
+        n = int(max(1, min(total, 10.0 / t1)))
         t0 = time.perf_counter()
-        oracle.gemm(a, b, rows=list(range(n)))
+        part(n)
         dt_s = time.perf_counter() - t0
+        share = n / total
+        if gemv:
+            value, unit = w.bytes(2) * share / dt_s / 1e9, "GB/s"
+        else:
+            value, unit = w.flops() * share / dt_s / 1e12, "TFLOP/s"
         result["cpu_baseline"] = {
-            "value": 2.0 * n * w.N * w.K / dt_s / 1e12, "unit": "TFLOP/s",
+            "value": value, "unit": unit,
             "cores": len(os.sched_getaffinity(0)), "kind": "oracle",
-            "sample": f"{n} of {w.M} rows of {w.name}, float64 numpy matmul, {dt_s:.1f} s wall"}
+            "sample": f"{n} of {total} {unit_name} of {w.name}, float64 numpy matmul, {dt_s:.1f} s wall"}
     print(json.dumps(result), flush=True)
 
 

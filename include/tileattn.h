@@ -181,8 +181,12 @@ ta_status mla_split_heuristic(int B, int H, int Hkv, int Skv, int *num_splits);
  *   B  device, bf16 [K, N] row-major         read only
  *   C  device, [M, N] row-major: fp32, or bf16 (rounded to nearest even) if
  *      c_bf16 != 0                             written
- *   M % 128 == 0, N % 128 == 0, K % 64 == 0 (else TA_ERR_UNSUPPORTED); every
- *   pointer 16-byte aligned; C must not overlap A or B; stream as attn_fwd.
+ *   M % 128 == 0, N % 128 == 0, K % 64 == 0, and K * N * 2 < 2^31 (else
+ *   TA_ERR_UNSUPPORTED, resp. TA_ERR_INVALID_SHAPE for the size); or M == 1,
+ *   the matrix-vector product of the paper's V0-V7 shapes (appendix table
+ *   "Matrix shapes in our benchmark"), with N % 64 == 0 and K % 8 == 0, which
+ *   runs a separate HBM-bound kernel on the vector ALUs; every pointer
+ *   16-byte aligned; C must not overlap A or B; stream as attn_fwd.
  * Status codes as attn_fwd; validation before any HIP call.
  */
 ta_status gemm_bf16(const void *A, const void *B, void *C, int c_bf16, int M, int N, int K,

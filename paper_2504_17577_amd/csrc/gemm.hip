@@ -268,6 +268,106 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
         }
 }
 
+// ---- M = 1: the matrix-vector product C[n] = sum_k a[k] B[k][n] ----------
+// (the paper's V0-V7 shapes).  B is read once and every byte of it feeds one
+// multiply-add, so this is HBM-bound and runs on the vector ALUs.  A
+// workgroup of 16 waves owns a strip of COLS columns (COLS * 2 contiguous
+// bytes of each B row); a lane reads 16 bytes (8 columns) of a row, so one
+// load instruction covers RPL = 512 / COLS full row segments.  Rows are taken
+// in groups of 8, split evenly over the waves; a wave walks its groups RPL
+// at a time, lane g (of RPL) taking all 8 rows of group gi + g, so that its
+// 8 values of a are one 16-byte load.  Partial sums meet in LDS and COLS
+// threads add them in a fixed order (results do not depend on timing).
+constexpr int GV_WAVES = 16;
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+template <int COLS, bool CBF16>
+__global__ __launch_bounds__(64 * GV_WAVES) void gemv_kernel(const uint16_t *A, const uint16_t *B,
+                                                              void *C, int N, int K)
+{
+    constexpr int LPR = COLS / 8;       // lanes per row segment
+    constexpr int RPL = 64 / LPR;       // row segments per load instruction
+    static_assert(RPL >= 1 && 8 % RPL == 0, "strip width");
+    __shared__ float red[GV_WAVES][RPL][COLS];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n0 = blockIdx.x * COLS;
+    const int g = lane / LPR;
+    const int c8 = (lane % LPR) * 8;    // this lane's first column in the strip
+    const int groups = K / 8;
+    const int g0 = (int)((int64_t)groups * wave / GV_WAVES);
+    const int g1 = (int)((int64_t)groups * (wave + 1) / GV_WAVES);
+
+    float acc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+        acc[i] = 0.f;
+    auto fma8 = [&](float x, const u32x4 &bv) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            acc[2 * i] = __builtin_fmaf(x, bf16_lo(bv[i]), acc[2 * i]);
+            acc[2 * i + 1] = __builtin_fmaf(x, bf16_hi(bv[i]), acc[2 * i + 1]);
+        }
+    };
+    int gi = g0;
+    for (; gi + RPL <= g1; gi += RPL) {
+        const size_t r0 = (size_t)8 * (gi + g);
+        const uint16_t *bp = B + r0 * N + n0 + c8;
+        u32x4 bv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            bv[u] = *(const u32x4 *)(bp + (size_t)u * N);
+        const u32x4 av = *(const u32x4 *)(A + r0);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            fma8((u & 1) ? bf16_hi(av[u >> 1]) : bf16_lo(av[u >> 1]), bv[u]);
+    }
+    // fewer than RPL groups left: one group at a time, lane g on its rows
+    // g, g + RPL, ... of the group
+    for (; gi < g1; ++gi)
+#pragma unroll
+        for (int h = 0; h < 8 / RPL; ++h) {
+            const size_t r = (size_t)8 * gi + h * RPL + g;
+            fma8(__uint_as_float((uint32_t)A[r] << 16), *(const u32x4 *)(B + r * N + n0 + c8));
+        }
+
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+        red[wave][g][c8 + i] = acc[i];
+    __syncthreads();
+    if (tid < COLS) {
+        float sum = 0.f;
+#pragma unroll
+        for (int w = 0; w < GV_WAVES; ++w)
+#pragma unroll
+            for (int r = 0; r < RPL; ++r)
+                sum += red[w][r][tid];
+        if (CBF16)
+            ((uint16_t *)C)[n0 + tid] = (uint16_t)pack_bf16(sum, 0.f);
+        else
+            ((float *)C)[n0 + tid] = sum;
+    }
+}
+
+// Strips of 256 columns (512-byte row segments) stream B faster than
+// 128-byte ones, but only when there are enough of them to give most CUs a
+// workgroup: measured 5.5-6.2 TB/s against 4.5-5.0 on the paper's N >= 36864
+// shapes, and 2.6-3.2 TB/s against 4.1-5.8 on N <= 16384.
+template <bool CBF16>
+hipError_t launch_gemv(const void *A, const void *B, void *C, int N, int K, hipStream_t s)
+{
+    const auto a = (const uint16_t *)A, b = (const uint16_t *)B;
+    if (N % 256 == 0 && N / 256 >= 144)
+        hipLaunchKernelGGL((gemv_kernel<256, CBF16>), dim3(N / 256), dim3(64 * GV_WAVES), 0, s,
+                           a, b, C, N, K);
+    else
+        hipLaunchKernelGGL((gemv_kernel<64, CBF16>), dim3(N / 64), dim3(64 * GV_WAVES), 0, s,
+                           a, b, C, N, K);
+    return hipGetLastError();
+}
+
 bool misaligned(const void *p) { return ((uintptr_t)p & 15u) != 0; }
 
 bool overlaps(const void *p, size_t pn, const void *q, size_t qn)
@@ -299,11 +399,13 @@ ta_status gemm_bf16(const void *A, const void *B, void *C, int c_bf16, int M, in
         return TA_ERR_NULL_POINTER;
     if (M < 1 || N < 1 || K < 1)
         return TA_ERR_INVALID_SHAPE;
-    if (M % 128 || N % 128 || K % BK)
+    const bool gemv = M == 1;
+    if (gemv ? (N % 64 || K % 8) : (M % 128 || N % 128 || K % BK))
         return TA_ERR_UNSUPPORTED;
-    // 32-bit offsets within a workgroup's tiles and buffer ranges
-    if ((int64_t)K * N * 2 >= (1ll << 31) || (int64_t)M * K >= (1ll << 40) ||
-        (int64_t)256 * K * 2 >= (1ll << 31))
+    // the tiled kernel: 32-bit offsets within a workgroup's tiles and buffer
+    // ranges (the matrix-vector kernel addresses with 64-bit pointers)
+    if (!gemv && ((int64_t)K * N * 2 >= (1ll << 31) || (int64_t)M * K >= (1ll << 40) ||
+                  (int64_t)256 * K * 2 >= (1ll << 31)))
         return TA_ERR_INVALID_SHAPE;
     if (misaligned(A) || misaligned(B) || misaligned(C))
         return TA_ERR_MISALIGNED;
@@ -319,6 +421,11 @@ ta_status gemm_bf16(const void *A, const void *B, void *C, int c_bf16, int M, in
     a.N = N;
     a.K = K;
     hipStream_t s = (hipStream_t)stream;
+    if (gemv) {
+        const hipError_t e = c_bf16 ? launch_gemv<true>(A, B, C, N, K, s)
+                                    : launch_gemv<false>(A, B, C, N, K, s);
+        return e == hipSuccess ? TA_OK : TA_ERR_LAUNCH;
+    }
     // 256 x 256 tiles when they give at least one workgroup per CU
     const bool big = M % 256 == 0 && N % 256 == 0 && (int64_t)(M / 256) * (N / 256) >= 256;
     const hipError_t e = big ? launch<256, 256>(a, c_bf16 != 0, s)

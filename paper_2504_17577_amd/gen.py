@@ -270,6 +270,16 @@ GEMM_WORKLOADS = {
         GemmWorkload("gemm_m5", 46, 8192, 8192, 8192),
         GemmWorkload("gemm_m6", 47, 8192, 28672, 8192),
         GemmWorkload("gemm_m7", 48, 8192, 8192, 28672),
+        # M = 1: the paper's matrix-vector shapes V0-V7 (same table)
+        GemmWorkload("gemv_tiny", 60, 1, 320, 200),
+        GemmWorkload("gemv_v0", 61, 1, 16384, 16384),
+        GemmWorkload("gemv_v1", 62, 1, 43008, 14336),
+        GemmWorkload("gemv_v2", 63, 1, 14336, 14336),
+        GemmWorkload("gemv_v3", 64, 1, 57344, 14336),
+        GemmWorkload("gemv_v4", 65, 1, 14336, 57344),
+        GemmWorkload("gemv_v5", 66, 1, 9216, 9216),
+        GemmWorkload("gemv_v6", 67, 1, 36864, 9216),
+        GemmWorkload("gemv_v7", 68, 1, 9216, 36864),
     )
 }
 
@@ -277,9 +287,13 @@ TENSOR_A, TENSOR_B = 5, 6
 
 
 def make_gemm_inputs(w: GemmWorkload, seed: int = 0):
-    """(a [M, K], b [K, N]) bfloat16 bit arrays for GEMM workload ``w``."""
-    return (normal_bf16((w.M, w.K), seed, w.wid, TENSOR_A),
-            normal_bf16((w.K, w.N), seed, w.wid, TENSOR_B))
+    """(a [M, K], b [K, N]) bfloat16 bit arrays for GEMM workload ``w``.
+    For M = 1 (up to 8.2e8 elements of B) B is drawn block-wise by the
+    thread pool of ``normal_bf16_blocks``."""
+    a = normal_bf16((w.M, w.K), seed, w.wid, TENSOR_A)
+    if w.M == 1:
+        return a, normal_bf16_blocks((w.K, w.N), seed, w.wid, TENSOR_B)
+    return a, normal_bf16((w.K, w.N), seed, w.wid, TENSOR_B)
 
 
 def random_gemm_problem(M: int, N: int, K: int, seed: int, wid: int = 102):

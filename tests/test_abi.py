@@ -233,6 +233,11 @@ BAD_GEMM = [
     (dict(M=200), 3), (dict(N=100), 3), (dict(K=96), 3),
     (dict(A=GA + 8), 4), (dict(C=GC + 4), 4),
     (dict(C=GA + 1024), 6), (dict(C=GB - 4096), 6), (dict(c_bf16=1, C=GB - 256 * 256 * 2 + 16), 6),
+    # M = 1 (matrix-vector): N % 64 and K % 8; other M still need M % 128
+    (dict(M=1, N=96), 3), (dict(M=1, K=12), 3), (dict(M=2), 3), (dict(M=1, C=GC + 4), 4),
+    (dict(M=1, C=GA + 128), 6),
+    # the tiled kernel's 32-bit offsets: K * N * 2 < 2^31
+    (dict(N=65536, K=16384), 2),
 ]
 
 

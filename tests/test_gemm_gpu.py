@@ -90,3 +90,57 @@ def test_gemm_rejects_bad_shapes(ta):
     with pytest.raises(ta.TileAttnError) as e:
         ta.gemm_bf16(dev(a), dev(b))
     assert e.value.status == 3
+
+
+# M = 1: the matrix-vector kernel (the paper's V0-V7 shapes)
+GEMV_SHAPES = [(64, 8), (320, 200), (1024, 4096), (4096, 1000), (192, 16392),
+               (36864, 72), (36864, 1048)]
+
+
+@pytest.mark.parametrize("shape", GEMV_SHAPES, ids=[str(s) for s in GEMV_SHAPES])
+def test_gemv_full_compare(ta, shape):
+    """N % 64 == 0, K % 8 == 0: strips of 64 columns (and of 256 from
+    N = 36864 on), row ranges split unevenly over the 16 waves when K / 8 is
+    not a multiple of 16, waves with no rows, and K tails shorter than the
+    unrolled step"""
+    N, K = shape
+    print(f"gemv N={N} K={K}", flush=True)
+    a, b = gen.random_gemm_problem(1, N, K, seed=N + K)
+    c = torch.full((1, N), float("nan"), device="cuda")
+    ta.gemm_bf16(dev(a), dev(b), out=c)
+    torch.cuda.synchronize()
+    check(f"gemv {shape}", c, a, b)
+
+
+@pytest.mark.parametrize("name", ["gemv_v5", "gemv_v7", "gemv_v0", "gemv_v6"])
+def test_gemv_workload_sampled(ta, name):
+    """The paper's matrix-vector shapes at full size: every output finite,
+    sampled columns (first and last of strips, random ones) against the
+    oracle on the same columns of B."""
+    w = gen.GEMM_WORKLOADS[name]
+    print(f"gemv workload {name} {w.describe()}", flush=True)
+    a, b = gen.make_gemm_inputs(w, seed=0)
+    c = torch.full((1, w.N), float("nan"), device="cuda")
+    ta.gemm_bf16(dev(a), dev(b), out=c)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(c).all())
+    rng = np.random.default_rng(2)
+    cols = sorted({0, 1, 63, 64, 127, w.N - 64, w.N - 1} | {int(x) for x in rng.integers(0, w.N, size=40)})
+    bs = np.ascontiguousarray(b[:, cols])
+    ref, scale = oracle.gemm(a, bs)[0], oracle.gemm_abs(a, bs)[0]
+    got = c[0, torch.tensor(cols)].cpu().numpy()
+    worst = float((np.abs(got - ref) / (REL_ABS * scale)).max())
+    print(f"{name}: worst err/tol={worst:.3f}", flush=True)
+    assert worst <= 1.0
+
+
+def test_gemv_bf16_out_and_deterministic(ta):
+    a, b = gen.random_gemm_problem(1, 2048, 3000, seed=11)
+    da, db = dev(a), dev(b)
+    c32 = ta.gemm_bf16(da, db)
+    c32b = ta.gemm_bf16(da, db)
+    c16 = ta.gemm_bf16(da, db, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert torch.equal(c32.view(torch.int32), c32b.view(torch.int32))
+    assert torch.equal(c16.view(torch.int16), c32.to(torch.bfloat16).view(torch.int16))
+    check("gemv bf16 out", c16, a, b, bf16=True)

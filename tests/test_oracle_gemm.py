@@ -47,3 +47,18 @@ def test_abs_scale_bounds_result():
     assert (np.abs(oracle.gemm(a, b)) <= oracle.gemm_abs(a, b) + 1e-12).all()
     ones = _bits(np.ones((3, 4)))
     assert np.array_equal(oracle.gemm_abs(ones, _bits(-np.ones((4, 2)))), np.full((3, 2), 4.0))
+
+
+def test_matrix_vector_is_dot_products():
+    """M = 1 (the paper's V0-V7 shapes): each output is one dot product,
+    evaluated here with math.fsum, and the column-sliced call the GPU tests
+    use gives the same values as the full one."""
+    a, b = gen.random_gemm_problem(1, 24, 520, seed=6)
+    c = oracle.gemm(a, b)
+    A, B = gen.f32_from_bf16(a).astype(float), gen.f32_from_bf16(b).astype(float)
+    assert c.shape == (1, 24)
+    for j in range(24):
+        ref = math.fsum(A[0, k] * B[k, j] for k in range(520))
+        assert abs(c[0, j] - ref) <= 1e-12 * math.fsum(abs(A[0, k] * B[k, j]) for k in range(520))
+    cols = [23, 0, 5]
+    assert np.array_equal(oracle.gemm(a, np.ascontiguousarray(b[:, cols]))[0], c[0, cols])
