@@ -158,8 +158,11 @@ __global__ __launch_bounds__(NT, 6) void chunk_state_kernel(StateArgs args)
     const StateArgs &a = args;
     constexpr int PASS = 32;
     constexpr int NPASS = SQ / PASS;
-    __shared__ __attribute__((aligned(16))) unsigned char bt[PASS * SN * 2];
-    __shared__ __attribute__((aligned(16))) unsigned char xt[PASS * SP * 2];
+    // the pass buffers (Bm 8 KB, x 4 KB) and, after the last pass, the
+    // staging of the result rows (32 rows of S, 16 KB) share one array
+    __shared__ __attribute__((aligned(16))) unsigned char smem[32 * SN * 4];
+    unsigned char *const bt = smem;
+    unsigned char *const xt = smem + PASS * SN * 2;
     __shared__ float wts[SQ];
     __shared__ float wsum[4];
     __shared__ float alast;
@@ -238,16 +241,28 @@ __global__ __launch_bounds__(NT, 6) void chunk_state_kernel(StateArgs args)
 
     // lane holds S^T[n][p] for p = 32 pb + lane % 32 and n = 32 wave + 8 j +
     // 4 (lane / 32) + 0..3: four consecutive n of row p of S
+    // written through LDS, 32 rows of S (512 bytes each) at a time, so that a
+    // store instruction covers two whole rows; 16-byte chunk q of staged row
+    // r sits at chunk q ^ r
     float *out = a.states + (((size_t)b * a.s.nc + c) * a.s.H + h) * (SP * SN);
     const int col = lane & 31, hl = lane >> 5;
 #pragma unroll
-    for (int pb = 0; pb < 2; ++pb)
+    for (int pb = 0; pb < 2; ++pb) {
+        __syncthreads();   // pass buffers / previous rows no longer read
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int p = 32 * pb + col, n = 32 * wave + 8 * j + 4 * hl;
-            *(float4 *)(out + p * SN + n) =
+            const int q = 8 * wave + 2 * j + hl;
+            *(float4 *)(smem + col * (SN * 4) + ((q ^ col) * 16)) =
                 float4{acc[pb][4 * j], acc[pb][4 * j + 1], acc[pb][4 * j + 2], acc[pb][4 * j + 3]};
         }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = 8 * wave + 2 * i + hl;
+            *(float4 *)(out + (32 * pb + r) * SN + 4 * col) =
+                *(const float4 *)(smem + r * (SN * 4) + ((col ^ r) * 16));
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
