@@ -275,8 +275,9 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
 // bytes of each B row); a lane reads 16 bytes (8 columns) of a row, so one
 // load instruction covers RPL = 512 / COLS full row segments.  Rows are taken
 // in groups of 8, split evenly over the waves; a wave walks its groups RPL
-// at a time, lane g (of RPL) taking all 8 rows of group gi + g, so that its
-// 8 values of a are one 16-byte load.  Partial sums meet in LDS and COLS
+// (or 2 RPL) at a time, lane g (of RPL) taking all 8 rows of group gi + g
+// (or 16 rows of groups gi + 2g, gi + 2g + 1), so that its values of a are
+// 16-byte loads.  Partial sums meet in LDS and COLS
 // threads add them in a fixed order (results do not depend on timing).
 constexpr int GV_WAVES = 16;
 
@@ -312,6 +313,27 @@ __global__ __launch_bounds__(64 * GV_WAVES) void gemv_kernel(const uint16_t *A, 
         }
     };
     int gi = g0;
+    // 64-column strips: two groups (16 rows) per lane and step, 16 loads in
+    // flight per lane; 256-column strips: one group
+    constexpr int GPL = COLS == 64 ? 2 : 1;
+    for (; gi + GPL * RPL <= g1; gi += GPL * RPL) {
+        const size_t r0 = (size_t)8 * (gi + GPL * g);
+        const uint16_t *bp = B + r0 * N + n0 + c8;
+        u32x4 bv[8 * GPL];
+#pragma unroll
+        for (int u = 0; u < 8 * GPL; ++u)
+            bv[u] = *(const u32x4 *)(bp + (size_t)u * N);
+        u32x4 av[GPL];
+#pragma unroll
+        for (int q = 0; q < GPL; ++q)
+            av[q] = *(const u32x4 *)(A + r0 + 8 * q);
+#pragma unroll
+        for (int u = 0; u < 8 * GPL; ++u) {
+            const uint32_t w = av[u >> 3][(u & 7) >> 1];
+            fma8((u & 1) ? bf16_hi(w) : bf16_lo(w), bv[u]);
+        }
+    }
+    // then single groups per lane while RPL of them are left
     for (; gi + RPL <= g1; gi += RPL) {
         const size_t r0 = (size_t)8 * (gi + g);
         const uint16_t *bp = B + r0 * N + n0 + c8;

@@ -93,7 +93,7 @@ def test_gemm_rejects_bad_shapes(ta):
 
 
 # M = 1: the matrix-vector kernel (the paper's V0-V7 shapes)
-GEMV_SHAPES = [(64, 8), (320, 200), (1024, 4096), (4096, 1000), (192, 16392),
+GEMV_SHAPES = [(64, 8), (320, 200), (1024, 4096), (4096, 1000), (192, 16392), (2048, 3080),
                (36864, 72), (36864, 1048)]
 
 
@@ -101,8 +101,8 @@ GEMV_SHAPES = [(64, 8), (320, 200), (1024, 4096), (4096, 1000), (192, 16392),
 def test_gemv_full_compare(ta, shape):
     """N % 64 == 0, K % 8 == 0: strips of 64 columns (and of 256 from
     N = 36864 on), row ranges split unevenly over the 16 waves when K / 8 is
-    not a multiple of 16, waves with no rows, and K tails shorter than the
-    unrolled step"""
+    not a multiple of 16, waves with no rows, and every mix of the two-group
+    step, the one-group step and the tail"""
     N, K = shape
     print(f"gemv N={N} K={K}", flush=True)
     a, b = gen.random_gemm_problem(1, N, K, seed=N + K)
