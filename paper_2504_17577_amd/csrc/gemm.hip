@@ -282,9 +282,21 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
 constexpr int GV_WAVES = 16;
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+// B is read exactly once per call.  When it is larger than the 256 MB
+// Infinity Cache it goes through non-temporal loads (measured 5.1 -> 5.7
+// TB/s at V0, 6.1 -> 6.8 at V3, 4.0 -> 4.2 at V7 against ordinary loads);
+// a smaller B is read with ordinary loads, so that calls repeated on the
+// same matrix can find it there (V5, 170 MB: 6.1 TB/s, 4.1 non-temporal).
+template <bool NT>
+__device__ __forceinline__ u32x4 ld_b(const uint16_t *p)
+{
+    if (NT)
+        return __builtin_nontemporal_load((const u32x4 *)p);
+    return *(const u32x4 *)p;
+}
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-template <int COLS, bool CBF16>
+template <int COLS, bool NT, bool CBF16>
 __global__ __launch_bounds__(64 * GV_WAVES) void gemv_kernel(const uint16_t *A, const uint16_t *B,
                                                               void *C, int N, int K)
 {
@@ -322,7 +334,7 @@ __global__ __launch_bounds__(64 * GV_WAVES) void gemv_kernel(const uint16_t *A, 
         u32x4 bv[8 * GPL];
 #pragma unroll
         for (int u = 0; u < 8 * GPL; ++u)
-            bv[u] = *(const u32x4 *)(bp + (size_t)u * N);
+            bv[u] = ld_b<NT>(bp + (size_t)u * N);
         u32x4 av[GPL];
 #pragma unroll
         for (int q = 0; q < GPL; ++q)
@@ -340,7 +352,7 @@ __global__ __launch_bounds__(64 * GV_WAVES) void gemv_kernel(const uint16_t *A, 
         u32x4 bv[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
-            bv[u] = *(const u32x4 *)(bp + (size_t)u * N);
+            bv[u] = ld_b<NT>(bp + (size_t)u * N);
         const u32x4 av = *(const u32x4 *)(A + r0);
 #pragma unroll
         for (int u = 0; u < 8; ++u)
@@ -352,7 +364,7 @@ __global__ __launch_bounds__(64 * GV_WAVES) void gemv_kernel(const uint16_t *A, 
 #pragma unroll
         for (int h = 0; h < 8 / RPL; ++h) {
             const size_t r = (size_t)8 * gi + h * RPL + g;
-            fma8(__uint_as_float((uint32_t)A[r] << 16), *(const u32x4 *)(B + r * N + n0 + c8));
+            fma8(__uint_as_float((uint32_t)A[r] << 16), ld_b<NT>(B + r * N + n0 + c8));
         }
 
 #pragma unroll
@@ -377,17 +389,27 @@ __global__ __launch_bounds__(64 * GV_WAVES) void gemv_kernel(const uint16_t *A, 
 // 128-byte ones, but only when there are enough of them to give most CUs a
 // workgroup: measured 5.5-6.2 TB/s against 4.5-5.0 on the paper's N >= 36864
 // shapes, and 2.6-3.2 TB/s against 4.1-5.8 on N <= 16384.
-template <bool CBF16>
-hipError_t launch_gemv(const void *A, const void *B, void *C, int N, int K, hipStream_t s)
+template <bool NT, bool CBF16>
+hipError_t launch_gemv(const uint16_t *a, const uint16_t *b, void *C, int N, int K, hipStream_t s)
 {
-    const auto a = (const uint16_t *)A, b = (const uint16_t *)B;
     if (N % 256 == 0 && N / 256 >= 144)
-        hipLaunchKernelGGL((gemv_kernel<256, CBF16>), dim3(N / 256), dim3(64 * GV_WAVES), 0, s,
+        hipLaunchKernelGGL((gemv_kernel<256, NT, CBF16>), dim3(N / 256), dim3(64 * GV_WAVES), 0, s,
                            a, b, C, N, K);
     else
-        hipLaunchKernelGGL((gemv_kernel<64, CBF16>), dim3(N / 64), dim3(64 * GV_WAVES), 0, s,
+        hipLaunchKernelGGL((gemv_kernel<64, NT, CBF16>), dim3(N / 64), dim3(64 * GV_WAVES), 0, s,
                            a, b, C, N, K);
     return hipGetLastError();
+}
+
+hipError_t run_gemv(const void *A, const void *B, void *C, bool c_bf16, int N, int K, hipStream_t s)
+{
+    const auto a = (const uint16_t *)A, b = (const uint16_t *)B;
+    const bool nt = (size_t)K * N * 2 > ((size_t)256 << 20);
+    if (nt)
+        return c_bf16 ? launch_gemv<true, true>(a, b, C, N, K, s)
+                      : launch_gemv<true, false>(a, b, C, N, K, s);
+    return c_bf16 ? launch_gemv<false, true>(a, b, C, N, K, s)
+                  : launch_gemv<false, false>(a, b, C, N, K, s);
 }
 
 bool misaligned(const void *p) { return ((uintptr_t)p & 15u) != 0; }
@@ -444,8 +466,7 @@ ta_status gemm_bf16(const void *A, const void *B, void *C, int c_bf16, int M, in
     a.K = K;
     hipStream_t s = (hipStream_t)stream;
     if (gemv) {
-        const hipError_t e = c_bf16 ? launch_gemv<true>(A, B, C, N, K, s)
-                                    : launch_gemv<false>(A, B, C, N, K, s);
+        const hipError_t e = run_gemv(A, B, C, c_bf16 != 0, N, K, s);
         return e == hipSuccess ? TA_OK : TA_ERR_LAUNCH;
     }
     // 256 x 256 tiles when they give at least one workgroup per CU

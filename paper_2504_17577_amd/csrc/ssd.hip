@@ -43,6 +43,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -134,6 +135,38 @@ __device__ __forceinline__ u32x4 load_row16(const uint16_t *p, bool keep)
     return keep ? v : u32x4{0u, 0u, 0u, 0u};
 }
 
+// The streams that are read or written exactly once per call (x, the
+// entering states, the outputs) go through non-temporal accesses when they
+// add up to more than twice the 256 MB Infinity Cache (STREAM); the operands
+// that every head of a group re-reads (Bm, Cm, cb) stay ordinary.  Measured
+// at B=64 L=2048: chunk scan 4.14 -> 4.37 TB/s, chunk state 4.40 -> 4.74.
+// Smaller calls keep ordinary accesses, so that calls repeated on the same
+// tensors can find part of them there (B=1 L=8192, 134 and 268 MB: chunk
+// state 4.46 TB/s, 3.65 non-temporal; chunk scan 3.40, 3.21).
+template <bool STREAM>
+__device__ __forceinline__ u32x4 ld_once(const uint16_t *p)
+{
+    if (STREAM)
+        return __builtin_nontemporal_load((const u32x4 *)p);
+    return *(const u32x4 *)p;
+}
+template <bool STREAM>
+__device__ __forceinline__ f32x4 ld_once(const float *p)
+{
+    if (STREAM)
+        return __builtin_nontemporal_load((const f32x4 *)p);
+    return *(const f32x4 *)p;
+}
+template <bool STREAM>
+__device__ __forceinline__ void st_once(float *p, f32x4 v)
+{
+    if (STREAM)
+        __builtin_nontemporal_store(v, (f32x4 *)p);
+    else
+        *(f32x4 *)p = v;
+}
+constexpr size_t STREAM_BYTES = (size_t)512 << 20;
+
 struct SsdShape {
     int B, L, H, G, nc;
     int hpg;   // H / G
@@ -149,6 +182,7 @@ struct StateArgs {
     float *states;
 };
 
+template <bool STREAM>
 __global__ __launch_bounds__(NT, 6) void chunk_state_kernel(StateArgs args)
 {
     // Positions are staged in passes of 32 (Bm 8 KB + weighted x 4 KB of LDS,
@@ -188,7 +222,7 @@ __global__ __launch_bounds__(NT, 6) void chunk_state_kernel(StateArgs args)
         const int p0 = c * SQ + k * PASS;
         nb0 = *(const u32x4 *)(bsrc + (size_t)min(p0 + rb0, a.s.L - 1) * brow);
         nb1 = *(const u32x4 *)(bsrc + (size_t)min(p0 + rb1, a.s.L - 1) * brow);
-        nx = *(const u32x4 *)(xsrc + (size_t)min(p0 + rx, a.s.L - 1) * xrow);
+        nx = ld_once<STREAM>(xsrc + (size_t)min(p0 + rx, a.s.L - 1) * xrow);
     };
     load_pass(0);
 
@@ -259,8 +293,8 @@ __global__ __launch_bounds__(NT, 6) void chunk_state_kernel(StateArgs args)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int r = 8 * wave + 2 * i + hl;
-            *(float4 *)(out + (32 * pb + r) * SN + 4 * col) =
-                *(const float4 *)(smem + r * (SN * 4) + ((col ^ r) * 16));
+            st_once<STREAM>(out + (32 * pb + r) * SN + 4 * col,
+                    *(const f32x4 *)(smem + r * (SN * 4) + ((col ^ r) * 16)));
         }
     }
 }
@@ -276,6 +310,7 @@ struct ScanArgs {
     float *out;
 };
 
+template <bool STREAM>
 __global__ __launch_bounds__(NT, 3) void chunk_scan_kernel(ScanArgs args)
 {
     const ScanArgs &a = args;
@@ -312,18 +347,18 @@ __global__ __launch_bounds__(NT, 3) void chunk_scan_kernel(ScanArgs args)
     for (int i = 0; i < SQ * 8 / NT; ++i) {
         const int q = i * NT + tid, r = q >> 3, cc = q & 7;
         const int tr = min(t0 + r, a.s.L - 1);
-        const u32x4 v = load_row16(a.x + ((size_t)b * a.s.L + tr) * xrow + (size_t)h * SP + cc * 8,
-                                   t0 + r < a.s.L);
+        const u32x4 xv = ld_once<STREAM>(a.x + ((size_t)b * a.s.L + tr) * xrow + (size_t)h * SP + cc * 8);
+        const u32x4 v = t0 + r < a.s.L ? xv : u32x4{0u, 0u, 0u, 0u};
         *(u32x4 *)(xt + r * (SP * 2) + ((cc ^ swz_tr128(r)) * 16)) = v;
     }
     const float *hin = a.prev + (((size_t)b * a.s.nc + c) * a.s.H + h) * (SP * SN);
 #pragma unroll
     for (int i = 0; i < SP * 16 / NT; ++i) {
         const int q = i * NT + tid, r = q >> 4, cc = q & 15;
-        const float4 f0 = *(const float4 *)(hin + r * SN + cc * 8);
-        const float4 f1 = *(const float4 *)(hin + r * SN + cc * 8 + 4);
-        const u32x4 v = {pack_bf16(f0.x, f0.y), pack_bf16(f0.z, f0.w), pack_bf16(f1.x, f1.y),
-                         pack_bf16(f1.z, f1.w)};
+        const f32x4 f0 = ld_once<STREAM>(hin + r * SN + cc * 8);
+        const f32x4 f1 = ld_once<STREAM>(hin + r * SN + cc * 8 + 4);
+        const u32x4 v = {pack_bf16(f0[0], f0[1]), pack_bf16(f0[2], f0[3]), pack_bf16(f1[0], f1[1]),
+                         pack_bf16(f1[2], f1[3])};
         *(u32x4 *)(ht + r * (SN * 2) + ((cc ^ swz_row256(r)) * 16)) = v;
     }
     __syncthreads();
@@ -495,10 +530,10 @@ __global__ __launch_bounds__(NT, 3) void chunk_scan_kernel(ScanArgs args)
 #pragma unroll
         for (int it = 0; it < 8; ++it) {
             const int r = 4 * it + (lane >> 4), q = lane & 15;
-            const float4 v = *(const float4 *)(stg + r * SP + ((q ^ (r & 15)) * 4));
+            const f32x4 v = *(const f32x4 *)(stg + r * SP + ((q ^ (r & 15)) * 4));
             const int tt = t0 + 32 * lbs[i] + r;
             if (tt < a.s.L)
-                *(float4 *)(a.out + ((size_t)b * a.s.L + tt) * xrow_ + (size_t)h * SP + 4 * q) = v;
+                st_once<STREAM>(a.out + ((size_t)b * a.s.L + tt) * xrow_ + (size_t)h * SP + 4 * q, v);
         }
     }
 }
@@ -663,7 +698,12 @@ ta_status ssd_chunk_state(const void *x, const void *Bm, const float *dt, const 
         overlaps(states, ns, A, (size_t)nheads * 4))
         return TA_ERR_ALIASING;
     StateArgs a{s, (const uint16_t *)x, (const uint16_t *)Bm, dt, A, states};
-    hipLaunchKernelGGL(chunk_state_kernel, dim3(s.B * s.nc * s.H), dim3(NT), 0, (hipStream_t)stream, a);
+    if (nx + ns > STREAM_BYTES)
+        hipLaunchKernelGGL(chunk_state_kernel<true>, dim3(s.B * s.nc * s.H), dim3(NT), 0,
+                           (hipStream_t)stream, a);
+    else
+        hipLaunchKernelGGL(chunk_state_kernel<false>, dim3(s.B * s.nc * s.H), dim3(NT), 0,
+                           (hipStream_t)stream, a);
     return launched(hipGetLastError());
 }
 
@@ -696,7 +736,13 @@ ta_status ssd_chunk_scan(const void *x, const void *Cm, const float *cb, const f
         if (overlaps(out, no, (const void *)in[0], in[1]))
             return TA_ERR_ALIASING;
     ScanArgs a{s, (const uint16_t *)x, (const uint16_t *)Cm, cb, dt, A, prev_states, D, out};
-    hipLaunchKernelGGL(chunk_scan_kernel, dim3(s.B * s.nc * s.H), dim3(NT), 0, (hipStream_t)stream, a);
+    // x, the entering states and y: the streams read or written once
+    if (nx * 2 + ins[5][1] + no > STREAM_BYTES)
+        hipLaunchKernelGGL(chunk_scan_kernel<true>, dim3(s.B * s.nc * s.H), dim3(NT), 0,
+                           (hipStream_t)stream, a);
+    else
+        hipLaunchKernelGGL(chunk_scan_kernel<false>, dim3(s.B * s.nc * s.H), dim3(NT), 0,
+                           (hipStream_t)stream, a);
     return launched(hipGetLastError());
 }
 
