@@ -34,6 +34,8 @@
 //    visited; only tiles crossing the diagonal or the end of the sequence
 //    take the masked path; there, waves whose queries see none of a tile
 //    skip it.
+//  * Epilogue: the normalised O rows are staged in LDS so that each store
+//    instruction writes whole rows.
 //  * Grid: one workgroup per (batch, head, query tile); the hardware deals
 //    consecutive workgroup ids round-robin to the 8 XCDs, so ids are
 //    remapped to give each XCD a contiguous range of heads (their K/V stay
@@ -473,30 +475,49 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(Args args)
     // epilogue: normalise, store O rows (fp32, or bf16 rounded to nearest
     // even) and LSE.  A row that saw no key of its split (only possible with
     // key splits) stores the empty partial result: O = 0, LSE = -inf.
+    //   The rows go through LDS so that every store instruction writes whole
+    // rows (lane (col, half) holds 4 consecutive dims of row col per (db, g):
+    // written directly, each instruction would be 32 pieces of 16 or 8
+    // bytes).  Each wave stages its 32 rows in its own quarter of the tile
+    // buffers, which every wave has left behind at the last tile's barrier;
+    // 16-byte chunk q of staged row r sits at q ^ (r % RCH).  A wave reads
+    // back only what it wrote itself (its LDS accesses complete in order).
     const float l = sum_halves(k.l_run);
-    if (k.qi < a.Sq) {
-        const bool empty = !(l > 0.f);
-        const float inv = empty ? 0.f : 1.f / l;
-        const size_t row = row0 + k.qi;
+    const bool empty = !(l > 0.f);
+    const float inv = empty ? 0.f : 1.f / l;
+    constexpr int EB = OBF16 ? 2 : 4;     // bytes per output element
+    constexpr int RCH = D * EB / 16;      // 16-byte chunks per row
+    constexpr int RPI = 64 / RCH;         // rows per store instruction
+    unsigned char *const stg = k.wave == 0 ? kb0 : k.wave == 1 ? kb1 : k.wave == 2 ? vb0 : vb1;
 #pragma unroll
-        for (int db = 0; db < C::DB; ++db)
+    for (int db = 0; db < C::DB; ++db)
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int d = 32 * db + 8 * g + 4 * k.half;
-                const float x0 = k.acc_o[db][4 * g + 0] * inv, x1 = k.acc_o[db][4 * g + 1] * inv;
-                const float x2 = k.acc_o[db][4 * g + 2] * inv, x3 = k.acc_o[db][4 * g + 3] * inv;
-                if (OBF16) {
-                    const u32x2 v = {pack_bf16(x0, x1), pack_bf16(x2, x3)};
-                    *(u32x2 *)((uint16_t *)a.O + row * D + d) = v;
-                } else {
-                    *(float4 *)((float *)a.O + (size_t)split * a.o_split + row * D + d) =
-                        float4{x0, x1, x2, x3};
-                }
-            }
-        if (k.half == 0)
-            a.LSE[(size_t)split * a.l_split + row] =
-                empty ? -INFINITY : (k.m_run + log2f(l)) * LN2;
+        for (int g = 0; g < 4; ++g) {
+            const int byte = (32 * db + 8 * g + 4 * k.half) * EB;   // within the row
+            unsigned char *p =
+                stg + k.col * (D * EB) + (((byte >> 4) ^ (k.col & (RCH - 1))) * 16) + (byte & 15);
+            const float x0 = k.acc_o[db][4 * g + 0] * inv, x1 = k.acc_o[db][4 * g + 1] * inv;
+            const float x2 = k.acc_o[db][4 * g + 2] * inv, x3 = k.acc_o[db][4 * g + 3] * inv;
+            if (OBF16)
+                *(u32x2 *)p = u32x2{pack_bf16(x0, x1), pack_bf16(x2, x3)};
+            else
+                *(float4 *)p = float4{x0, x1, x2, x3};
+        }
+#pragma unroll
+    for (int it = 0; it < 32 / RPI; ++it) {
+        const int r = it * RPI + k.lane / RCH, q = k.lane % RCH;
+        const u32x4 v = *(const u32x4 *)(stg + r * (D * EB) + ((q ^ (r & (RCH - 1))) * 16));
+        const int qr = q0 + k.wave * 32 + r;
+        if (qr < a.Sq) {
+            if (OBF16)
+                *(u32x4 *)((uint16_t *)a.O + (row0 + qr) * D + 8 * q) = v;
+            else
+                *(u32x4 *)((float *)a.O + (size_t)split * a.o_split + (row0 + qr) * D + 4 * q) = v;
+        }
     }
+    if (k.qi < a.Sq && k.half == 0)
+        a.LSE[(size_t)split * a.l_split + row0 + k.qi] =
+            empty ? -INFINITY : (k.m_run + log2f(l)) * LN2;
 }
 
 template <int D, bool CAUSAL, bool OBF16>
