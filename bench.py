@@ -4,7 +4,10 @@ A step is one attn_fwd launch over one batch of the workload, inputs already
 resident in HBM.  Prints ONE JSON line with the throughput in TFLOP/s (matmul
 flops over visible query-key pairs), the roofline position of the kernel
 against the dense bf16 MFMA peak, and the fp64 CPU oracle's throughput on a
-bounded sample of the same workload as a reported baseline.
+bounded sample of the same workload as a reported baseline.  The oracle is
+touched only in that CPU leg, after the timed region: it spot-checks a few
+outputs (a failed check ends the run without a number) and times itself;
+--no-cpu-baseline skips the leg and never loads the oracle.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--out f32|bf16]
                   [--splits 1|N|auto] [--no-cpu-baseline]
@@ -215,8 +218,6 @@ def mla_cpu_baseline(w, q, q_pe, kv, k_pe, budget_s: float = 15.0):
 
 def bench_mla(args, torch, tileattn):
     """One MLA decode step per launch (plus the split merge when split)."""
-    import oracle
-
     w = gen.MLA_WORKLOADS[args.workload]
     q, q_pe, kv, k_pe = gen.make_mla_inputs(w, seed=args.seed)
     dq, dqp, dkv, dkp = (to_device(x, torch) for x in (q, q_pe, kv, k_pe))
@@ -235,13 +236,6 @@ def bench_mla(args, torch, tileattn):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    rows = [(0, 0), (w.B - 1, w.H - 1), (w.B // 2, w.H // 2)]
-    ro, rl = oracle.mla_rows(q, q_pe, kv, k_pe, w.scale, rows)
-    idx = tuple(torch.tensor(c) for c in zip(*rows))
-    err_o = float(np.abs(o[idx].cpu().numpy() - ro).max())
-    err_l = float(np.abs(lse[idx].cpu().numpy() - rl).max())
-    if not (err_o <= 2e-2 and err_l <= 1e-3):
-        raise SystemExit(f"bench: result check failed (max|dO|={err_o}, max|dLSE|={err_l})")
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -269,9 +263,18 @@ def bench_mla(args, torch, tileattn):
                      "traffic": None, "hbm_gbs_algorithmic": round(gbs, 1),
                      "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)},
         "wall_s_timed": round(wall, 4),
-        "check": {"max_abs_dO": err_o, "max_abs_dLSE": err_l, "rows": len(rows)},
     }
     if not args.no_cpu_baseline:
+        # the CPU-oracle leg: spot check, then the oracle's throughput
+        import oracle
+        rows = [(0, 0), (w.B - 1, w.H - 1), (w.B // 2, w.H // 2)]
+        ro, rl = oracle.mla_rows(q, q_pe, kv, k_pe, w.scale, rows)
+        idx = tuple(torch.tensor(c) for c in zip(*rows))
+        err_o = float(np.abs(o[idx].cpu().numpy() - ro).max())
+        err_l = float(np.abs(lse[idx].cpu().numpy() - rl).max())
+        if not (err_o <= 2e-2 and err_l <= 1e-3):
+            raise SystemExit(f"bench: result check failed (max|dO|={err_o}, max|dLSE|={err_l})")
+        result["check"] = {"max_abs_dO": err_o, "max_abs_dLSE": err_l, "rows": len(rows)}
         result["cpu_baseline"] = mla_cpu_baseline(w, q, q_pe, kv, k_pe)
     print(json.dumps(result), flush=True)
 
@@ -283,8 +286,6 @@ GEMV_METRIC = "matrix-vector product throughput (algorithmic HBM GB/s), 1 GPU"
 def bench_gemm(args, torch, tileattn):
     """C = A B at a GEMM workload; torch.matmul (hipBLASLt) on the same
     operands is timed the same way as a reference."""
-    import oracle
-
     w = gen.GEMM_WORKLOADS[args.workload]
     a, b = gen.make_gemm_inputs(w, seed=args.seed)
     da, db = to_device(a, torch), to_device(b, torch)
@@ -312,24 +313,6 @@ def bench_gemm(args, torch, tileattn):
 
     ms, wall = timed(step)
     gemv = w.M == 1
-    if gemv:
-        # M = 1: sampled columns (the oracle would widen all of B otherwise)
-        rng = np.random.default_rng(args.seed + 1)
-        cols = np.unique(np.concatenate([[0, 63, 64, w.N - 1], rng.integers(0, w.N, size=60)]))
-        bs = np.ascontiguousarray(b[:, cols])
-        ref, scale = oracle.gemm(a, bs)[0], oracle.gemm_abs(a, bs)[0]
-        got = c.float()[0, torch.from_numpy(cols).cuda()].cpu().numpy()
-        checked = {"columns": int(len(cols))}
-    else:
-        rows = [0, w.M // 2, w.M - 1]
-        ref = oracle.gemm(a, b, rows=rows)
-        scale = oracle.gemm_abs(a, b, rows=rows)
-        got = c.float()[torch.tensor(rows)].cpu().numpy()
-        checked = {"rows": len(rows)}
-    tol = 1e-5 * scale + (2.0 ** -8 * np.abs(ref) if c_bf16 else 0.0)
-    worst = float((np.abs(got - ref) / tol).max())
-    if not worst <= 1.0:
-        raise SystemExit(f"bench: result check failed (worst err/tol {worst})")
     ref_out = torch.empty((w.M, w.N), dtype=torch.bfloat16, device="cuda")
     ms_ref, _ = timed(lambda: torch.matmul(da, db, out=ref_out))
     tflops = w.flops() / (ms * 1e-3) / 1e12
@@ -361,9 +344,30 @@ def bench_gemm(args, torch, tileattn):
                              "ms_per_call": round(ms_ref, 5),
                              "ratio": round(ms_ref / ms, 4)},
         "wall_s_timed": round(wall, 4),
-        "check": {"worst_err_over_tol": worst, **checked},
     })
     if not args.no_cpu_baseline:
+        # the CPU-oracle leg: spot check of the output, then the oracle's
+        # throughput
+        import oracle
+        if gemv:
+            # M = 1: sampled columns (the oracle would widen all of B otherwise)
+            rng = np.random.default_rng(args.seed + 1)
+            cols = np.unique(np.concatenate([[0, 63, 64, w.N - 1], rng.integers(0, w.N, size=60)]))
+            bs = np.ascontiguousarray(b[:, cols])
+            ref, scale = oracle.gemm(a, bs)[0], oracle.gemm_abs(a, bs)[0]
+            got = c.float()[0, torch.from_numpy(cols).cuda()].cpu().numpy()
+            checked = {"columns": int(len(cols))}
+        else:
+            rows = [0, w.M // 2, w.M - 1]
+            ref = oracle.gemm(a, b, rows=rows)
+            scale = oracle.gemm_abs(a, b, rows=rows)
+            got = c.float()[torch.tensor(rows)].cpu().numpy()
+            checked = {"rows": len(rows)}
+        tol = 1e-5 * scale + (2.0 ** -8 * np.abs(ref) if c_bf16 else 0.0)
+        worst = float((np.abs(got - ref) / tol).max())
+        if not worst <= 1.0:
+            raise SystemExit(f"bench: result check failed (worst err/tol {worst})")
+        result["check"] = {"worst_err_over_tol": worst, **checked}
         # fp64 oracle on a bounded share of the output (about 10 s), calibrated
         # on a small share after one untimed call (the first pays numpy's set-up)
         if gemv:
@@ -403,8 +407,6 @@ def bench_ssd(args, torch, tileattn):
     chunk_state) at an SSD workload.  Its other inputs (states, the chunk
     matrix) are made beforehand on the GPU by the library's own chunk-state,
     state-passing and chunk-matrix kernels."""
-    import oracle.ssd as ossd
-
     op = args.op or "chunk_scan"
     w = gen.SSD_WORKLOADS[args.workload]
     inp = gen.make_ssd_inputs(w, seed=args.seed)
@@ -427,30 +429,6 @@ def bench_ssd(args, torch, tileattn):
     step()
     torch.cuda.synchronize()
 
-    # spot check two (batch, head) slices against the oracle's own chain
-    Q = w.Q
-    worst = 0.0
-    for b, h in ((0, 0), (w.B - 1, w.H - 1)):
-        g = h // (w.H // w.G)
-        sub = dict(x=inp["x"][b:b + 1, :, [h]], Bm=inp["Bm"][b:b + 1, :, [g]],
-                   Cm=inp["Cm"][b:b + 1, :, [g]], dt=inp["dt"][b:b + 1, :, [h]],
-                   A=inp["A"][[h]], D=inp["D"][[h]])
-        if op == "chunk_scan":
-            ref, _ = ossd.ssd_forward(sub["x"], sub["dt"], sub["A"], sub["Bm"], sub["Cm"], sub["D"], Q)
-            ab = lambda u: np.ascontiguousarray(u) & np.uint16(0x7FFF)
-            s_abs = ossd.chunk_state_abs(sub["x"], sub["Bm"], sub["dt"], sub["A"], Q)
-            p_abs, _ = ossd.state_passing(s_abs, sub["dt"], sub["A"], Q)
-            cb_abs = ossd.bmm_chunk(ab(sub["Cm"]), ab(sub["Bm"]), Q)
-            scale = ossd.chunk_scan_abs(sub["x"], sub["Cm"], cb_abs, sub["dt"], sub["A"], p_abs,
-                                        sub["D"], Q)
-            got, bound = y[b:b + 1, :, [h]].cpu().numpy(), 2.0 ** -6
-        else:
-            ref = ossd.chunk_state(sub["x"], sub["Bm"], sub["dt"], sub["A"], Q)
-            scale = ossd.chunk_state_abs(sub["x"], sub["Bm"], sub["dt"], sub["A"], Q)
-            got, bound = states[b:b + 1, :, [h]].cpu().numpy(), 2.0 ** -7
-        worst = max(worst, float((np.abs(got - ref) / np.maximum(scale, 1e-30)).max() / bound))
-    if not worst <= 1.0:
-        raise SystemExit(f"bench: result check failed (worst err/bound {worst})")
 
     for _ in range(args.warmup):
         step()
@@ -478,9 +456,35 @@ def bench_ssd(args, torch, tileattn):
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None},
         "wall_s_timed": round(wall, 4),
-        "check": {"worst_err_over_bound": worst, "slices": 2},
     }
     if not args.no_cpu_baseline:
+        # the CPU-oracle leg: spot check, then the oracle's throughput
+        import oracle.ssd as ossd
+        # spot check two (batch, head) slices against the oracle's own chain
+        Q = w.Q
+        worst = 0.0
+        for b, h in ((0, 0), (w.B - 1, w.H - 1)):
+            g = h // (w.H // w.G)
+            sub = dict(x=inp["x"][b:b + 1, :, [h]], Bm=inp["Bm"][b:b + 1, :, [g]],
+                       Cm=inp["Cm"][b:b + 1, :, [g]], dt=inp["dt"][b:b + 1, :, [h]],
+                       A=inp["A"][[h]], D=inp["D"][[h]])
+            if op == "chunk_scan":
+                ref, _ = ossd.ssd_forward(sub["x"], sub["dt"], sub["A"], sub["Bm"], sub["Cm"], sub["D"], Q)
+                ab = lambda u: np.ascontiguousarray(u) & np.uint16(0x7FFF)
+                s_abs = ossd.chunk_state_abs(sub["x"], sub["Bm"], sub["dt"], sub["A"], Q)
+                p_abs, _ = ossd.state_passing(s_abs, sub["dt"], sub["A"], Q)
+                cb_abs = ossd.bmm_chunk(ab(sub["Cm"]), ab(sub["Bm"]), Q)
+                scale = ossd.chunk_scan_abs(sub["x"], sub["Cm"], cb_abs, sub["dt"], sub["A"], p_abs,
+                                            sub["D"], Q)
+                got, bound = y[b:b + 1, :, [h]].cpu().numpy(), 2.0 ** -6
+            else:
+                ref = ossd.chunk_state(sub["x"], sub["Bm"], sub["dt"], sub["A"], Q)
+                scale = ossd.chunk_state_abs(sub["x"], sub["Bm"], sub["dt"], sub["A"], Q)
+                got, bound = states[b:b + 1, :, [h]].cpu().numpy(), 2.0 ** -7
+            worst = max(worst, float((np.abs(got - ref) / np.maximum(scale, 1e-30)).max() / bound))
+        if not worst <= 1.0:
+            raise SystemExit(f"bench: result check failed (worst err/bound {worst})")
+        result["check"] = {"worst_err_over_bound": worst, "slices": 2}
         # the oracle's chain on whole (batch, head) slices, about 10 s
         def one(b, h):
             g = h // (w.H // w.G)
@@ -589,16 +593,6 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # spot check a few rows against the oracle so a broken build cannot post a number
-    import oracle
-    rows = [(0, 0, 0), (w.B - 1, w.Hq - 1, w.Sq - 1), (w.B // 2, w.Hq // 2, w.Sq // 2)]
-    ro, rl = oracle.attn_rows(q, k, v, w.causal, w.scale, rows)
-    idx = tuple(torch.tensor(c) for c in zip(*rows))
-    err_o = float(np.abs(o[idx].float().cpu().numpy() - ro).max())
-    err_l = float(np.abs(lse[idx].cpu().numpy() - rl).max())
-    if not (err_o <= 2e-2 and err_l <= 1e-3):
-        raise SystemExit(f"bench: result check failed (max|dO|={err_o}, max|dLSE|={err_l})")
-
     # timed region: K launches on this stream between two HIP events
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
@@ -644,7 +638,6 @@ def main():
             "hbm_gbs_algorithmic": round(w.bytes(2 if o_bf16 else 4) / (ms * 1e-3) / 1e9, 1),
         },
         "wall_s_timed": round(wall, 4),
-        "check": {"max_abs_dO": err_o, "max_abs_dLSE": err_l, "rows": len(rows)},
     }
     if args.sustain > 0:
         with PowerSampler() as sampler:
@@ -660,6 +653,17 @@ def main():
                     **sustained(torch, lambda: torch.matmul(ga, gb, out=gc), 2.0 * n ** 3,
                                 args.sustain, sampler)}
     if not args.no_cpu_baseline:
+        # the CPU-oracle leg: a spot check of a few rows (so that a broken
+        # build cannot post a number), then the oracle's own throughput
+        import oracle
+        rows = [(0, 0, 0), (w.B - 1, w.Hq - 1, w.Sq - 1), (w.B // 2, w.Hq // 2, w.Sq // 2)]
+        ro, rl = oracle.attn_rows(q, k, v, w.causal, w.scale, rows)
+        idx = tuple(torch.tensor(c) for c in zip(*rows))
+        err_o = float(np.abs(o[idx].float().cpu().numpy() - ro).max())
+        err_l = float(np.abs(lse[idx].cpu().numpy() - rl).max())
+        if not (err_o <= 2e-2 and err_l <= 1e-3):
+            raise SystemExit(f"bench: result check failed (max|dO|={err_o}, max|dLSE|={err_l})")
+        result["check"] = {"max_abs_dO": err_o, "max_abs_dLSE": err_l, "rows": len(rows)}
         result["cpu_baseline"] = cpu_baseline(w, q, k, v)
     print(json.dumps(result), flush=True)
 
