@@ -65,6 +65,28 @@ def test_workload_full_compare(ta, name):
     compare_full(ta, q, k, v, w.causal, w.scale, name)
 
 
+@pytest.mark.parametrize("name", ["dense_d128_s2k", "causal_peaky_d128_s8k", "gqa4_causal_d128_s4k"])
+def test_workload_full_size_every_element(ta, name):
+    """The three large configurations of the attention target at full size,
+    every element of O and LSE against the fp64 oracle (all rows; the oracle
+    is the multi-threaded C one, about 5-10 s per configuration on 16
+    cores).  Prints max |dO|, its 99.9th percentile and location, and max
+    |dLSE|."""
+    w = gen.WORKLOADS[name]
+    print(f"{name}: {w.describe()}, every element", flush=True)
+    q, k, v = gen.make_inputs(w, seed=0)
+    o, lse = run(ta, q, k, v, w.causal, w.scale)
+    ro, rl = oracle.attn_fwd(q, k, v, w.causal, w.scale)
+    o, lse = o.cpu().numpy(), lse.cpu().numpy()
+    assert np.isfinite(o).all() and np.isfinite(lse).all(), f"{name}: unwritten or non-finite output"
+    do = np.abs(o - ro)
+    eo, el = float(do.max()), float(np.abs(lse - rl).max())
+    at = np.unravel_index(int(do.argmax()), do.shape)
+    print(f"{name}: max|dO|={eo:.3e} at (b, h, i, d)={tuple(int(x) for x in at)}, "
+          f"p99.9|dO|={float(np.quantile(do, 0.999)):.3e}, max|dLSE|={el:.3e}", flush=True)
+    assert eo <= O_TOL and el <= LSE_TOL, name
+
+
 def sample_rows(w, rng, n_random):
     """Rows to check at full size: tile edges, first/last rows, random rows."""
     rows = set()
