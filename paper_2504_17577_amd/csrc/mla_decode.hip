@@ -146,17 +146,14 @@ __device__ __forceinline__ u32x4s buffer_rsrc(const void *base, uint32_t bytes)
 
 // One 16-byte-per-lane DMA: lane l's 16 bytes at byte `voff` of the buffer
 // land at LDS address `lds` + 16 l (`lds` wave-uniform).
-// M0 (which the compiler reserves) is saved and restored around the load.
+// M0 is an operand of the statement, so the compiler sets it (and keeps any
+// value of its own) around the load.
 __device__ __forceinline__ void dma16(uint32_t lds, uint32_t voff, u32x4s rsrc)
 {
-    uint32_t saved;
-    asm volatile("s_mov_b32 %0, m0\n\t"
-                 "s_mov_b32 m0, %1\n\t"
-                 "s_nop 0\n\t"
-                 "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
-                 "s_mov_b32 m0, %0"
-                 : "=&s"(saved)
-                 : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(rsrc)
+    asm volatile("s_nop 0\n\t"   // one wait state between the M0 write and the load
+                 "buffer_load_dwordx4 %0, %1, 0 offen lds"
+                 :
+                 : "v"(voff), "s"(rsrc), "{m0}"(__builtin_amdgcn_readfirstlane(lds))
                  : "memory");
 }
 
