@@ -206,6 +206,21 @@ def test_permutation_invariance(ta):
     assert float((o1 - o2).abs().max()) <= O_TOL and float((l1 - l2).abs().max()) <= LSE_TOL
 
 
+def test_causal_row_equals_prefix(ta):
+    """P9: causal row i (bottom-right aligned, Sq = Sk) is the non-causal
+    result of query i over keys 0..i.  The two launches may raise the running
+    max at different tiles (the decision is per wave), so the weights can round
+    differently: compared within the stated tolerances, not bitwise."""
+    q, k, v = gen.random_problem(1, 2, 2, 300, 300, 128, seed=12)
+    scale = 1 / math.sqrt(128)
+    o, lse = run(ta, q, k, v, True, scale)
+    for i in (0, 1, 63, 64, 150, 299):
+        op, lp = run(ta, np.ascontiguousarray(q[:, :, i:i + 1]), np.ascontiguousarray(k[:, :, :i + 1]),
+                     np.ascontiguousarray(v[:, :, :i + 1]), False, scale)
+        assert float((o[:, :, i] - op[:, :, 0]).abs().max()) <= O_TOL, i
+        assert float((lse[:, :, i] - lp[:, :, 0]).abs().max()) <= LSE_TOL, i
+
+
 def test_deterministic_and_side_stream(ta):
     q, k, v = gen.random_problem(2, 4, 4, 700, 700, 128, seed=9)
     o1, l1 = run(ta, q, k, v, True, 0.088388)
