@@ -182,83 +182,101 @@ struct StateArgs {
     float *states;
 };
 
-template <bool STREAM>
-__global__ __launch_bounds__(NT, 6) void chunk_state_kernel(StateArgs args)
+// One workgroup per (batch, chunk, HPW heads of one group).  The heads share
+// the Bm operand (read once for all of them), and a position's x slice of
+// the HPW heads is HPW * 128 contiguous bytes, read whole: two heads per
+// workgroup measured 4.73 -> 5.35 TB/s at B=64 L=2048 against one (128-byte
+// row pieces, Bm read per head), four heads 5.25 (two waves per SIMD).
+// Positions are staged in passes of 32 (Bm 8 KB + HPW weighted x tiles of 4
+// KB in LDS, so several workgroups share a CU and cover each other's memory
+// latency); the global loads of pass k + 1 are issued into registers before
+// the MFMAs of pass k.  The result rows go through LDS, 32 rows of S (512
+// bytes each) at a time, so that a store instruction covers two whole rows;
+// 16-byte chunk q of staged row r sits at chunk q ^ r.
+template <int HPW, bool STREAM>
+__global__ __launch_bounds__(NT, HPW >= 4 ? 2 : HPW == 2 ? 4 : 6) void chunk_state_kernel(StateArgs args)
 {
-    // Positions are staged in passes of 32 (Bm 8 KB + weighted x 4 KB of LDS,
-    // so many workgroups share a CU and cover each other's memory latency);
-    // the global loads of pass k + 1 are issued into registers before the
-    // MFMAs of pass k.
     const StateArgs &a = args;
     constexpr int PASS = 32;
     constexpr int NPASS = SQ / PASS;
-    // the pass buffers (Bm 8 KB, x 4 KB) and, after the last pass, the
-    // staging of the result rows (32 rows of S, 16 KB) share one array
-    __shared__ __attribute__((aligned(16))) unsigned char smem[32 * SN * 4];
+    constexpr int XT = PASS * SP * 2;                       // one head's x tile of a pass
+    constexpr int PASS_BYTES = PASS * SN * 2 + HPW * XT;
+    constexpr int STG_BYTES = 32 * SN * 4;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[PASS_BYTES > STG_BYTES ? PASS_BYTES : STG_BYTES];
     unsigned char *const bt = smem;
     unsigned char *const xt = smem + PASS * SN * 2;
-    __shared__ float wts[SQ];
+    __shared__ float wts[HPW][SQ];
     __shared__ float wsum[4];
-    __shared__ float alast;
+    __shared__ float alast[HPW];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int n_wg = a.s.B * a.s.nc * a.s.H;
+    const int hgs = a.s.H / HPW;
+    const int n_wg = a.s.B * a.s.nc * hgs;
     const int logical = xcd_logical(blockIdx.x, n_wg);
-    const int h = logical % a.s.H;
-    const int c = (logical / a.s.H) % a.s.nc;
-    const int b = logical / (a.s.H * a.s.nc);
-    const int g = h / a.s.hpg;
+    const int h0 = (logical % hgs) * HPW;
+    const int c = (logical / hgs) % a.s.nc;
+    const int b = logical / (hgs * a.s.nc);
+    const int g = h0 / a.s.hpg;
 
-    // per-thread staging slots of a pass: two 16-byte chunks of Bm (rows of
-    // 16 chunks) and one of x (rows of 8 chunks)
-    const size_t brow = (size_t)a.s.G * SN;          // Bm elements per position
-    const size_t xrow = (size_t)a.s.H * SP;          // x elements per position
+    const size_t brow = (size_t)a.s.G * SN;
+    const size_t xrow = (size_t)a.s.H * SP;
     const int rb0 = tid >> 4, rb1 = (NT + tid) >> 4, cb_ = tid & 15;
-    const int rx = tid >> 3, cx = tid & 7;
     const uint16_t *bsrc = a.Bm + (size_t)b * a.s.L * brow + (size_t)g * SN + cb_ * 8;
-    const uint16_t *xsrc = a.x + (size_t)b * a.s.L * xrow + (size_t)h * SP + cx * 8;
-    u32x4 nb0, nb1, nx;
+    const uint16_t *xbase = a.x + (size_t)b * a.s.L * xrow + (size_t)h0 * SP;
+    // x chunk i of this thread: row (i NT + tid) / (8 HPW), chunk (i NT + tid) % (8 HPW)
+    u32x4 nb0, nb1, nx[HPW];
     auto load_pass = [&](int k) {
         const int p0 = c * SQ + k * PASS;
         nb0 = *(const u32x4 *)(bsrc + (size_t)min(p0 + rb0, a.s.L - 1) * brow);
         nb1 = *(const u32x4 *)(bsrc + (size_t)min(p0 + rb1, a.s.L - 1) * brow);
-        nx = ld_once<STREAM>(xsrc + (size_t)min(p0 + rx, a.s.L - 1) * xrow);
+#pragma unroll
+        for (int i = 0; i < HPW; ++i) {
+            const int q = i * NT + tid, r = q / (8 * HPW), cc = q % (8 * HPW);
+            nx[i] = ld_once<STREAM>(xbase + (size_t)min(p0 + r, a.s.L - 1) * xrow + cc * 8);
+        }
     };
     load_pass(0);
 
-    // cumulative log-decay of this chunk and the per-position weights
     const int t = c * SQ + tid;
-    const float dtv = a.dt[((size_t)b * a.s.L + min(t, a.s.L - 1)) * a.s.H + h];
-    const float dtl = t < a.s.L ? dtv : 0.f;
-    const float cum = block_scan(dtl * a.A[h], wsum);
-    if (tid == NT - 1)
-        alast = cum;
-    __syncthreads();
-    const float a_last = alast;
-    wts[tid] = exp2f((a_last - cum) * LOG2E) * dtl;   // 0 past L
+    const bool tv = t < a.s.L;
+#pragma unroll
+    for (int hi = 0; hi < HPW; ++hi) {
+        const float dtv = a.dt[((size_t)b * a.s.L + min(t, a.s.L - 1)) * a.s.H + h0 + hi];
+        const float dtl = tv ? dtv : 0.f;
+        const float cum = block_scan(dtl * a.A[h0 + hi], wsum);
+        if (tid == NT - 1)
+            alast[hi] = cum;
+        __syncthreads();   // alast visible; wsum free for the next head
+        wts[hi][tid] = exp2f((alast[hi] - cum) * LOG2E) * dtl;
+    }
 
-    f32x16 acc[2];
+    f32x16 acc[HPW][2];
 #pragma unroll
-    for (int pb = 0; pb < 2; ++pb)
+    for (int hi = 0; hi < HPW; ++hi)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-            acc[pb][r] = 0.f;
+        for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[hi][pb][r] = 0.f;
 
     for (int k = 0; k < NPASS; ++k) {
-        __syncthreads();   // wts visible; the previous pass's operand reads done
+        __syncthreads();
         const int p0 = c * SQ + k * PASS;
-        // Bm rows past L are zeroed (they would meet a zero weight anyway,
-        // but the masked product must not see arbitrary bits)
         *(u32x4 *)(bt + rb0 * (SN * 2) + ((cb_ ^ swz_tr256(rb0)) * 16)) =
             p0 + rb0 < a.s.L ? nb0 : u32x4{0u, 0u, 0u, 0u};
         *(u32x4 *)(bt + rb1 * (SN * 2) + ((cb_ ^ swz_tr256(rb1)) * 16)) =
             p0 + rb1 < a.s.L ? nb1 : u32x4{0u, 0u, 0u, 0u};
-        const float w = wts[k * PASS + rx];
-        u32x4 v;
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-            v[e] = pack_bf16(bf16_lo(nx[e]) * w, bf16_hi(nx[e]) * w);
-        *(u32x4 *)(xt + rx * (SP * 2) + ((cx ^ swz_tr128(rx)) * 16)) = v;
+        for (int i = 0; i < HPW; ++i) {
+            const int q = i * NT + tid, r = q / (8 * HPW), cc = q % (8 * HPW);
+            const int hi = cc / 8, pc = cc % 8;
+            const float w = wts[hi][k * PASS + r];
+            u32x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                v[e] = pack_bf16(bf16_lo(nx[i][e]) * w, bf16_hi(nx[i][e]) * w);
+            *(u32x4 *)(xt + hi * XT + r * (SP * 2) + ((pc ^ swz_tr128(r)) * 16)) = v;
+        }
         __syncthreads();
         if (k + 1 < NPASS)
             load_pass(k + 1);
@@ -266,35 +284,36 @@ __global__ __launch_bounds__(NT, 6) void chunk_state_kernel(StateArgs args)
         for (int ks = 0; ks < PASS / 16; ++ks) {
             const bf16x8 av = tr_operand<SN * 2, swz_tr256>(bt, 16 * ks, 32 * wave, lane);
 #pragma unroll
-            for (int pb = 0; pb < 2; ++pb) {
-                const bf16x8 bv = tr_operand<SP * 2, swz_tr128>(xt, 16 * ks, 32 * pb, lane);
-                acc[pb] = mfma32(av, bv, acc[pb]);
-            }
+            for (int hi = 0; hi < HPW; ++hi)
+#pragma unroll
+                for (int pb = 0; pb < 2; ++pb) {
+                    const bf16x8 bv = tr_operand<SP * 2, swz_tr128>(xt + hi * XT, 16 * ks, 32 * pb, lane);
+                    acc[hi][pb] = mfma32(av, bv, acc[hi][pb]);
+                }
         }
     }
 
-    // lane holds S^T[n][p] for p = 32 pb + lane % 32 and n = 32 wave + 8 j +
-    // 4 (lane / 32) + 0..3: four consecutive n of row p of S
-    // written through LDS, 32 rows of S (512 bytes each) at a time, so that a
-    // store instruction covers two whole rows; 16-byte chunk q of staged row
-    // r sits at chunk q ^ r
-    float *out = a.states + (((size_t)b * a.s.nc + c) * a.s.H + h) * (SP * SN);
     const int col = lane & 31, hl = lane >> 5;
 #pragma unroll
-    for (int pb = 0; pb < 2; ++pb) {
-        __syncthreads();   // pass buffers / previous rows no longer read
+    for (int hi = 0; hi < HPW; ++hi) {
+        float *out = a.states + (((size_t)b * a.s.nc + c) * a.s.H + h0 + hi) * (SP * SN);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int q = 8 * wave + 2 * j + hl;
-            *(float4 *)(smem + col * (SN * 4) + ((q ^ col) * 16)) =
-                float4{acc[pb][4 * j], acc[pb][4 * j + 1], acc[pb][4 * j + 2], acc[pb][4 * j + 3]};
-        }
-        __syncthreads();
+        for (int pb = 0; pb < 2; ++pb) {
+            __syncthreads();
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int r = 8 * wave + 2 * i + hl;
-            st_once<STREAM>(out + (32 * pb + r) * SN + 4 * col,
-                    *(const f32x4 *)(smem + r * (SN * 4) + ((col ^ r) * 16)));
+            for (int j = 0; j < 4; ++j) {
+                const int q = 8 * wave + 2 * j + hl;
+                *(float4 *)(smem + col * (SN * 4) + ((q ^ col) * 16)) =
+                    float4{acc[hi][pb][4 * j], acc[hi][pb][4 * j + 1], acc[hi][pb][4 * j + 2],
+                           acc[hi][pb][4 * j + 3]};
+            }
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = 8 * wave + 2 * i + hl;
+                st_once<STREAM>(out + (32 * pb + r) * SN + 4 * col,
+                                *(const f32x4 *)(smem + r * (SN * 4) + ((col ^ r) * 16)));
+            }
         }
     }
 }
@@ -698,12 +717,24 @@ ta_status ssd_chunk_state(const void *x, const void *Bm, const float *dt, const 
         overlaps(states, ns, A, (size_t)nheads * 4))
         return TA_ERR_ALIASING;
     StateArgs a{s, (const uint16_t *)x, (const uint16_t *)Bm, dt, A, states};
-    if (nx + ns > STREAM_BYTES)
-        hipLaunchKernelGGL(chunk_state_kernel<true>, dim3(s.B * s.nc * s.H), dim3(NT), 0,
-                           (hipStream_t)stream, a);
-    else
-        hipLaunchKernelGGL(chunk_state_kernel<false>, dim3(s.B * s.nc * s.H), dim3(NT), 0,
-                           (hipStream_t)stream, a);
+    // two heads per workgroup when a group holds an even number of heads and
+    // the grid keeps at least four workgroups per CU (smaller grids run
+    // faster with one head each: B=1 L=2048 2.85 against 3.12 TB/s)
+    const bool strm = nx + ns > STREAM_BYTES;
+    const hipStream_t hs = (hipStream_t)stream;
+    if (s.hpg % 2 == 0 && (int64_t)s.B * s.nc * (s.H / 2) >= 1024) {
+        const dim3 grid(s.B * s.nc * (s.H / 2));
+        if (strm)
+            hipLaunchKernelGGL((chunk_state_kernel<2, true>), grid, dim3(NT), 0, hs, a);
+        else
+            hipLaunchKernelGGL((chunk_state_kernel<2, false>), grid, dim3(NT), 0, hs, a);
+    } else {
+        const dim3 grid(s.B * s.nc * s.H);
+        if (strm)
+            hipLaunchKernelGGL((chunk_state_kernel<1, true>), grid, dim3(NT), 0, hs, a);
+        else
+            hipLaunchKernelGGL((chunk_state_kernel<1, false>), grid, dim3(NT), 0, hs, a);
+    }
     return launched(hipGetLastError());
 }
 

@@ -197,6 +197,28 @@ def test_workload_b1_s8k_sampled(ta):
           ossd.chunk_scan_abs(*args))
 
 
+def test_chunk_state_two_heads_per_workgroup(ta):
+    """Grids of at least 1024 two-head workgroups run two heads of a group
+    per workgroup: both heads of several pairs, both groups, a ragged last
+    chunk, against the oracle on those heads alone."""
+    shape = (2, 4000, 64, 2)
+    print(f"ssd_chunk_state {shape} (two heads per workgroup)", flush=True)
+    w, inp = problem(shape, seed=21)
+    out = torch.full((w.B, w.nc, w.H, w.P, w.N), float("nan"), device="cuda")
+    ta.ssd_chunk_state(dev_bf16(inp["x"]), dev_bf16(inp["Bm"]), dev_f32(inp["dt"]),
+                       dev_f32(inp["A"]), out=out)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(out).all())
+    heads = [0, 1, 30, 31, 32, 33, 62, 63]
+    groups = [h // (w.H // w.G) for h in heads]
+    sub_x, sub_dt, sub_A = inp["x"][:, :, heads], inp["dt"][:, :, heads], inp["A"][heads]
+    for i, (h, g) in enumerate(zip(heads, groups)):
+        bm = inp["Bm"][:, :, [g]]
+        ref = ossd.chunk_state(sub_x[:, :, [i]], bm, sub_dt[:, :, [i]], sub_A[[i]], Q)
+        scale = ossd.chunk_state_abs(sub_x[:, :, [i]], bm, sub_dt[:, :, [i]], sub_A[[i]], Q)
+        check(f"chunk_state {shape} head {h}", out[:, :, [h]].cpu().numpy(), ref, scale)
+
+
 def test_repeatable_and_stream(ta):
     """Two runs are bitwise identical; a non-default stream gives the same."""
     w, inp = problem((1, 600, 4, 2), seed=31)
