@@ -105,6 +105,33 @@ def test_mla_workload_sampled(ta, name):
     assert eo <= O_TOL and el <= LSE_TOL
 
 
+def test_mla_cache_beyond_32_bits(ta):
+    """A latent cache of more than 2^31 elements (over 4 GiB), so that any
+    32-bit element or byte offset into it would wrap: heads of the batch
+    elements on either side of the 2^30- and 2^31-element boundaries, and of
+    the last one, against the oracle (each batch element is its own B = 1
+    problem there)."""
+    B, H, Skv = 132, 128, 32768
+    assert B * Skv * 512 > 2 ** 31
+    q, q_pe = (gen.normal_bf16_blocks(s, seed=0, wid=111, tensor=t)
+               for t, s in ((0, (B, H, 512)), (1, (B, H, 64))))
+    kv = gen.normal_bf16_blocks((B, Skv, 1, 512), seed=0, wid=111, tensor=2)
+    k_pe = gen.normal_bf16_blocks((B, Skv, 1, 64), seed=0, wid=111, tensor=3)
+    scale = 576 ** -0.5
+    n = ta.mla_split_heuristic(B, H, 1, Skv)
+    print(f"mla cache beyond 32 bits: B={B} H={H} Skv={Skv}, {n} splits", flush=True)
+    o, lse = run(ta, q, q_pe, kv, k_pe, scale, n)
+    # batch element b starts at element b * Skv * 512 = b * 2^24
+    for b in (0, 63, 64, 127, 128, B - 1):
+        heads = [0, 1, 31, 32, 63, 64, 100, 127]
+        ro, rl = oracle.mla_rows(q[b:b + 1], q_pe[b:b + 1], kv[b:b + 1], k_pe[b:b + 1], scale,
+                                 [(0, h) for h in heads])
+        eo = float(np.abs(o[b, heads].cpu().numpy() - ro).max())
+        el = float(np.abs(lse[b, heads].cpu().numpy() - rl).max())
+        print(f"  batch {b}: max|dO|={eo:.3e} max|dLSE|={el:.3e}", flush=True)
+        assert eo <= O_TOL and el <= LSE_TOL, b
+
+
 def test_mla_single_position(ta):
     """One cache position: O is that latent row.  The weight is exp2 of the
     fp32 residual of (score * c) - round(score * c), so it and the row sum are

@@ -133,6 +133,36 @@ def test_workload_full_size_sampled(ta, name):
     assert eo <= O_TOL and el <= LSE_TOL, name
 
 
+def test_offsets_beyond_32_bits(ta):
+    """Q, K, V and O each hold more than 2^31 elements (O over 2^33 bytes), so
+    any 32-bit element or byte offset in the kernel would wrap.  Every row of
+    the heads on either side of the 2^31-element, 2^31-byte and 2^32-byte
+    boundaries, and of the last head, against the oracle (each head is its
+    own B = H = 1 problem there)."""
+    B, H, S, D = 1040, 32, 512, 128
+    assert B * H * S * D > 2 ** 31
+    q, k, v = (gen.normal_bf16_blocks((B, H, S, D), seed=0, wid=110, tensor=t) for t in range(3))
+    dq, dk, dv = dev(q), dev(k), dev(v)
+    o = torch.full((B, H, S, D), float("nan"), dtype=torch.float32, device="cuda")
+    lse = torch.full((B, H, S), float("nan"), dtype=torch.float32, device="cuda")
+    # (b, h) whose first row starts at or just before each boundary:
+    # row offset (b H + h) S crosses 2^22 (2^31 bytes of fp32 O), 2^23
+    # (2^32 bytes of O) and 2^24 (2^31 elements of every tensor)
+    heads = [(0, 0), (255, 31), (256, 0), (511, 31), (512, 0), (1023, 31), (1024, 0), (B - 1, H - 1)]
+    scale = 1 / math.sqrt(D)
+    for causal in (False, True):
+        print(f"offsets beyond 32 bits: B={B} H={H} S={S} D={D} causal={causal}", flush=True)
+        ta.attn_fwd(dq, dk, dv, causal=causal, scale=scale, out=o, lse=lse)
+        torch.cuda.synchronize()
+        for b, h in heads:
+            sl = (slice(b, b + 1), slice(h, h + 1))
+            ro, rl = oracle.attn_fwd(q[sl], k[sl], v[sl], causal, scale)
+            go, gl = o[sl].cpu().numpy(), lse[sl].cpu().numpy()
+            eo, el = float(np.abs(go - ro).max()), float(np.abs(gl - rl).max())
+            report(f"causal={causal} head (b, h)=({b}, {h})", eo, el)
+            assert eo <= O_TOL and el <= LSE_TOL, (causal, b, h)
+
+
 EDGE = [
     # (B, Hq, Hkv, Sq, Sk, D, causal)
     (1, 1, 1, 1, 1, 64, False), (1, 1, 1, 1, 1, 128, True),
