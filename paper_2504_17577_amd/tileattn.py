@@ -139,6 +139,19 @@ def attn_fwd_bf16out_raw(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale, 
                                   float(scale), stream)
 
 
+def _one_device(*tensors):
+    """A context that makes the tensors' device current for the launch (the
+    library launches on the current device); raises if they are spread over
+    several devices."""
+    import torch
+
+    dev = tensors[0].device
+    for t in tensors[1:]:
+        if t is not None and t.device != dev:
+            raise TypeError(f"all tensors must be on one device ({dev} and {t.device} given)")
+    return torch.cuda.device(dev)
+
+
 def _attn(q, k, v, causal, scale, out, lse, stream, o_dtype, raw):
     import torch
 
@@ -162,8 +175,9 @@ def _attn(q, k, v, causal, scale, out, lse, stream, o_dtype, raw):
             raise TypeError(f"{name} must be a contiguous {dt} tensor of shape {shape}")
     if stream is None:
         stream = torch.cuda.current_stream(q.device)
-    rc = raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
-             B, Hq, Hkv, Sq, Sk, D, causal, scale, stream.cuda_stream)
+    with _one_device(q, k, v, out, lse):
+        rc = raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
+                 B, Hq, Hkv, Sq, Sk, D, causal, scale, stream.cuda_stream)
     if rc != TA_OK:
         raise TileAttnError(rc, ta_status_string(rc))
     return out, lse
@@ -208,10 +222,16 @@ def attn_fwd_split(q, k, v, causal: bool = False, scale: float | None = None,
     if num_splits is None:
         num_splits = ta_split_heuristic(B, Hq, Hkv, Sq, Sk, D, causal)
     need = ta_split_workspace_bytes(B, Hq, Sq, D, num_splits)
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device)
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
-    if workspace.dtype != torch.uint8 or not workspace.is_cuda or not workspace.is_contiguous():
-        raise TypeError("workspace must be a contiguous uint8 GPU tensor")
+        # freed when this call returns: keep the allocator from handing the
+        # block to other work before the launch on ``stream`` has finished
+        workspace.record_stream(stream)
+    if (workspace.dtype != torch.uint8 or workspace.device != q.device
+            or not workspace.is_contiguous()):
+        raise TypeError("workspace must be a contiguous uint8 tensor on q's device")
     ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel()
 
     def raw(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale, stream):
@@ -276,15 +296,18 @@ def mla_decode(q, q_pe, kv, k_pe, scale: float | None = None, num_splits: int | 
         if t.dtype != torch.float32 or tuple(t.shape) != shape or not t.is_contiguous():
             raise TypeError(f"{name} must be a contiguous float32 tensor of shape {shape}")
     need = mla_workspace_bytes(B, H, num_splits)
-    if workspace is None:
-        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
-    if workspace.dtype != torch.uint8 or not workspace.is_cuda or not workspace.is_contiguous():
-        raise TypeError("workspace must be a contiguous uint8 GPU tensor")
     if stream is None:
         stream = torch.cuda.current_stream(q.device)
-    rc = mla_decode_raw(q.data_ptr(), q_pe.data_ptr(), kv.data_ptr(), k_pe.data_ptr(),
-                        out.data_ptr(), lse.data_ptr(), B, H, Hkv, Skv, Dl, Dr, scale,
-                        num_splits, workspace.data_ptr(), workspace.numel(), stream.cuda_stream)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+        workspace.record_stream(stream)   # as in attn_fwd_split
+    if workspace.dtype != torch.uint8 or not workspace.is_cuda or not workspace.is_contiguous():
+        raise TypeError("workspace must be a contiguous uint8 GPU tensor")
+    with _one_device(q, q_pe, kv, k_pe, out, lse, workspace):
+        rc = mla_decode_raw(q.data_ptr(), q_pe.data_ptr(), kv.data_ptr(), k_pe.data_ptr(),
+                            out.data_ptr(), lse.data_ptr(), B, H, Hkv, Skv, Dl, Dr, scale,
+                            num_splits, workspace.data_ptr(), workspace.numel(),
+                            stream.cuda_stream)
     if rc != TA_OK:
         raise TileAttnError(rc, ta_status_string(rc))
     return out, lse
@@ -316,8 +339,9 @@ def gemm_bf16(a, b, out=None, out_dtype=None, stream=None):
         raise TypeError(f"out must be a contiguous {dt} tensor of shape {(M, N)}")
     if stream is None:
         stream = torch.cuda.current_stream(a.device)
-    rc = gemm_bf16_raw(a.data_ptr(), b.data_ptr(), out.data_ptr(), dt == torch.bfloat16, M, N, K,
-                       stream.cuda_stream)
+    with _one_device(a, b, out):
+        rc = gemm_bf16_raw(a.data_ptr(), b.data_ptr(), out.data_ptr(), dt == torch.bfloat16, M, N,
+                           K, stream.cuda_stream)
     if rc != TA_OK:
         raise TileAttnError(rc, ta_status_string(rc))
     return out
@@ -362,9 +386,10 @@ def ssd_chunk_state(x, Bm, dt, A, out=None, stream=None):
         out = torch.empty((Bsz, nc, H, P, N), dtype=torch.float32, device=x.device)
     _ssd_check("out", out, torch.float32, (Bsz, nc, H, P, N))
     stream = stream or torch.cuda.current_stream(x.device)
-    _ssd_raise(lib().ssd_chunk_state(x.data_ptr(), Bm.data_ptr(), dt.data_ptr(), A.data_ptr(),
-                                     out.data_ptr(), Bsz, L, H, G, P, N, SSD_CHUNK,
-                                     stream.cuda_stream))
+    with _one_device(x, Bm, dt, A, out):
+        _ssd_raise(lib().ssd_chunk_state(x.data_ptr(), Bm.data_ptr(), dt.data_ptr(), A.data_ptr(),
+                                         out.data_ptr(), Bsz, L, H, G, P, N, SSD_CHUNK,
+                                         stream.cuda_stream))
     return out
 
 
@@ -387,9 +412,10 @@ def ssd_state_passing(states, dt, A, prev=None, final=None, stream=None):
     _ssd_check("prev", prev, torch.float32, (Bsz, nc, H, P, N))
     _ssd_check("final", final, torch.float32, (Bsz, H, P, N))
     stream = stream or torch.cuda.current_stream(states.device)
-    _ssd_raise(lib().ssd_state_passing(states.data_ptr(), dt.data_ptr(), A.data_ptr(),
-                                       prev.data_ptr(), final.data_ptr(), Bsz, L, H, P, N,
-                                       SSD_CHUNK, stream.cuda_stream))
+    with _one_device(states, dt, A, prev, final):
+        _ssd_raise(lib().ssd_state_passing(states.data_ptr(), dt.data_ptr(), A.data_ptr(),
+                                           prev.data_ptr(), final.data_ptr(), Bsz, L, H, P, N,
+                                           SSD_CHUNK, stream.cuda_stream))
     return prev, final
 
 
@@ -405,8 +431,9 @@ def ssd_bmm_chunk(Cm, Bm, out=None, stream=None):
         out = torch.empty((Bsz, nc, G, SSD_CHUNK, SSD_CHUNK), dtype=torch.float32, device=Cm.device)
     _ssd_check("out", out, torch.float32, (Bsz, nc, G, SSD_CHUNK, SSD_CHUNK))
     stream = stream or torch.cuda.current_stream(Cm.device)
-    _ssd_raise(lib().ssd_bmm_chunk(Cm.data_ptr(), Bm.data_ptr(), out.data_ptr(), Bsz, L, G, N,
-                                   SSD_CHUNK, stream.cuda_stream))
+    with _one_device(Cm, Bm, out):
+        _ssd_raise(lib().ssd_bmm_chunk(Cm.data_ptr(), Bm.data_ptr(), out.data_ptr(), Bsz, L, G, N,
+                                       SSD_CHUNK, stream.cuda_stream))
     return out
 
 
@@ -427,10 +454,11 @@ def ssd_chunk_scan(x, Cm, cb, dt, A, prev_states, D=None, out=None, stream=None)
         out = torch.empty((Bsz, L, H, P), dtype=torch.float32, device=x.device)
     _ssd_check("out", out, torch.float32, (Bsz, L, H, P))
     stream = stream or torch.cuda.current_stream(x.device)
-    _ssd_raise(lib().ssd_chunk_scan(x.data_ptr(), Cm.data_ptr(), cb.data_ptr(), dt.data_ptr(),
-                                    A.data_ptr(), prev_states.data_ptr(),
-                                    D.data_ptr() if D is not None else None, out.data_ptr(),
-                                    Bsz, L, H, G, P, N, SSD_CHUNK, stream.cuda_stream))
+    with _one_device(x, Cm, cb, dt, A, prev_states, D, out):
+        _ssd_raise(lib().ssd_chunk_scan(x.data_ptr(), Cm.data_ptr(), cb.data_ptr(), dt.data_ptr(),
+                                        A.data_ptr(), prev_states.data_ptr(),
+                                        D.data_ptr() if D is not None else None, out.data_ptr(),
+                                        Bsz, L, H, G, P, N, SSD_CHUNK, stream.cuda_stream))
     return out
 
 

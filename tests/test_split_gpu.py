@@ -130,3 +130,27 @@ def test_split_rejects_small_workspace(ta):
     with pytest.raises(ta.TileAttnError) as e:
         ta.attn_fwd_split(dev(q), dev(k), dev(v), num_splits=4, workspace=ws)
     assert e.value.status == 8
+
+
+def test_split_side_stream_with_its_own_workspace(ta):
+    """attn_fwd_split and mla_decode on a non-default stream, each allocating
+    its workspace: the same bits as on the default stream, while the default
+    stream allocates and fills memory of the workspace's size right after the
+    launch (the freed workspace block must not be handed to it before the
+    side-stream kernels have finished)."""
+    q, k, v = (dev(a) for a in gen.random_problem(2, 8, 8, 512, 4000, 128, seed=31))
+    o_ref, l_ref = ta.attn_fwd_split(q, k, v, num_splits=6)
+    mq, mqp, mkv, mkp = (dev(a) for a in gen.random_mla_problem(4, 128, 1, 3000, seed=32))
+    mo_ref, ml_ref = ta.mla_decode(mq, mqp, mkv, mkp, num_splits=5)
+    need = max(ta.ta_split_workspace_bytes(2, 8, 512, 128, 6), ta.mla_workspace_bytes(4, 128, 5))
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    # launched on s from the default stream: outputs and workspaces are
+    # allocated on the default stream, whose next allocation follows
+    o, lse = ta.attn_fwd_split(q, k, v, num_splits=6, stream=s)
+    mo, ml = ta.mla_decode(mq, mqp, mkv, mkp, num_splits=5, stream=s)
+    junk = torch.full((need // 4 + 1,), float("nan"), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    del junk
+    assert torch.equal(o, o_ref) and torch.equal(lse, l_ref)
+    assert torch.equal(mo, mo_ref) and torch.equal(ml, ml_ref)
