@@ -6,8 +6,10 @@ flops over visible query-key pairs), the roofline position of the kernel
 against the dense bf16 MFMA peak, and the fp64 CPU oracle's throughput on a
 bounded sample of the same workload as a reported baseline.  The oracle is
 touched only in that CPU leg, after the timed region: it spot-checks a few
-outputs (a failed check ends the run without a number) and times itself;
---no-cpu-baseline skips the leg and never loads the oracle.
+outputs, times itself, and (attention and MLA) compares every row it
+computed with the last timed launch's output (a failed check ends the run
+without a number); --no-cpu-baseline skips the leg and never loads the
+oracle.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--out f32|bf16]
                   [--splits 1|N|auto] [--no-cpu-baseline]
@@ -97,10 +99,10 @@ def cpu_baseline(w, q, k, v, budget_s: float = 15.0):
     n_heads = int(max(1, min(w.B * w.Hq - 1, budget_s / max(t1, 1e-6) - 1)))
     rows = np.concatenate([head_rows(1 + i) for i in range(n_heads)]) if n_heads else None
     t0 = time.perf_counter()
-    oracle.attn_rows(q, k, v, w.causal, w.scale, rows, nthreads=threads, lib=lib)
+    ro, rl = oracle.attn_rows(q, k, v, w.causal, w.scale, rows, nthreads=threads, lib=lib)
     dt = time.perf_counter() - t0
     flops = w.flops() / (w.B * w.Hq) * n_heads
-    return {
+    info = {
         "value": flops / dt / 1e12,
         "unit": "TFLOP/s",
         "cores": threads,
@@ -108,6 +110,7 @@ def cpu_baseline(w, q, k, v, budget_s: float = 15.0):
         "sample": f"{n_heads} of {w.B * w.Hq} heads of {w.name} (all {w.Sq} query rows each), "
                   f"fp64 C oracle, {dt:.1f} s wall",
     }
+    return info, rows, ro, rl
 
 
 class PowerSampler:
@@ -208,12 +211,13 @@ def mla_cpu_baseline(w, q, q_pe, kv, k_pe, budget_s: float = 15.0):
     n_b = int(max(1, min(w.B - 1, budget_s / max(t1, 1e-6) - 1)))
     rows = [r for b in range(1, 1 + n_b) for r in heads(b)]
     t0 = time.perf_counter()
-    oracle.mla_rows(q, q_pe, kv, k_pe, w.scale, rows, nthreads=threads, lib=lib)
+    ro, rl = oracle.mla_rows(q, q_pe, kv, k_pe, w.scale, rows, nthreads=threads, lib=lib)
     dt = time.perf_counter() - t0
     flops = w.flops() / w.B * n_b
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+    info = {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": f"{n_b} of {w.B} batch elements of {w.name} (all {w.H} heads each), "
                       f"fp64 C oracle, {dt:.1f} s wall"}
+    return info, rows, ro, rl
 
 
 def bench_mla(args, torch, tileattn):
@@ -274,8 +278,16 @@ def bench_mla(args, torch, tileattn):
         err_l = float(np.abs(lse[idx].cpu().numpy() - rl).max())
         if not (err_o <= 2e-2 and err_l <= 1e-3):
             raise SystemExit(f"bench: result check failed (max|dO|={err_o}, max|dLSE|={err_l})")
-        result["check"] = {"max_abs_dO": err_o, "max_abs_dLSE": err_l, "rows": len(rows)}
-        result["cpu_baseline"] = mla_cpu_baseline(w, q, q_pe, kv, k_pe)
+        info, rows2, ro, rl = mla_cpu_baseline(w, q, q_pe, kv, k_pe)
+        # every head the oracle leg computed, against the last timed launch
+        idx = tuple(torch.tensor(c) for c in zip(*rows2))
+        err_o = max(err_o, float(np.abs(o[idx].cpu().numpy() - ro).max()))
+        err_l = max(err_l, float(np.abs(lse[idx].cpu().numpy() - rl).max()))
+        if not (err_o <= 2e-2 and err_l <= 1e-3):
+            raise SystemExit(f"bench: result check failed (max|dO|={err_o}, max|dLSE|={err_l})")
+        result["check"] = {"max_abs_dO": err_o, "max_abs_dLSE": err_l,
+                           "rows": len(rows) + len(rows2)}
+        result["cpu_baseline"] = info
     print(json.dumps(result), flush=True)
 
 
@@ -654,7 +666,8 @@ def main():
                                 args.sustain, sampler)}
     if not args.no_cpu_baseline:
         # the CPU-oracle leg: a spot check of a few rows (so that a broken
-        # build cannot post a number), then the oracle's own throughput
+        # build cannot post a number), then the oracle's own throughput on
+        # whole heads, whose rows are compared as well
         import oracle
         rows = [(0, 0, 0), (w.B - 1, w.Hq - 1, w.Sq - 1), (w.B // 2, w.Hq // 2, w.Sq // 2)]
         ro, rl = oracle.attn_rows(q, k, v, w.causal, w.scale, rows)
@@ -663,8 +676,16 @@ def main():
         err_l = float(np.abs(lse[idx].cpu().numpy() - rl).max())
         if not (err_o <= 2e-2 and err_l <= 1e-3):
             raise SystemExit(f"bench: result check failed (max|dO|={err_o}, max|dLSE|={err_l})")
-        result["check"] = {"max_abs_dO": err_o, "max_abs_dLSE": err_l, "rows": len(rows)}
-        result["cpu_baseline"] = cpu_baseline(w, q, k, v)
+        info, rows, ro, rl = cpu_baseline(w, q, k, v)
+        # the rows the oracle leg computed, every element of them, against
+        # the output of the last timed launch
+        idx = tuple(torch.from_numpy(np.ascontiguousarray(rows[:, c])) for c in range(3))
+        err_o = max(err_o, float(np.abs(o[idx].float().cpu().numpy() - ro).max()))
+        err_l = max(err_l, float(np.abs(lse[idx].cpu().numpy() - rl).max()))
+        if not (err_o <= 2e-2 and err_l <= 1e-3):
+            raise SystemExit(f"bench: result check failed (max|dO|={err_o}, max|dLSE|={err_l})")
+        result["check"] = {"max_abs_dO": err_o, "max_abs_dLSE": err_l, "rows": 3 + len(rows)}
+        result["cpu_baseline"] = info
     print(json.dumps(result), flush=True)
 
 
