@@ -72,6 +72,9 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
 // otherwise drain the loads in flight before every LDS read, unable to tell
 // which buffer they write); the loop waits for it with vmcnt(0).
 __device__ __forceinline__ void wait_dma_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// wait until at most N of this thread's tile loads are outstanding (N < 16)
+template <int N>
+__device__ __forceinline__ void wait_dma_upto() { __builtin_amdgcn_s_waitcnt(0x0F70 | N); }
 
 typedef uint32_t u32x4s __attribute__((ext_vector_type(4)));
 
@@ -111,16 +114,22 @@ struct Cfg {
     static constexpr int A_PER_THREAD = BM * (BK / 8) / NT;   // 16-byte slots
     static constexpr int B_PER_THREAD = BK * (BN / 8) / NT;
     static constexpr int BCH = BN / 8;                    // 16-byte chunks per B row
+    static constexpr int PER_STAGE = A_PER_THREAD + B_PER_THREAD;   // loads per thread
 };
 
-template <int BM, int BN, bool CBF16>
+// ST stages of A and B tiles in LDS: two (double buffering, one tile in
+// flight during the MFMAs) or a ring of three or four (ST - 1 tiles in
+// flight) for grids of at most one workgroup per CU, where no other
+// workgroup's MFMAs cover the wait for a tile.
+template <int BM, int BN, int ST, bool CBF16>
 __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
 {
     using C = Cfg<BM, BN>;
-    __shared__ __attribute__((aligned(16))) unsigned char a0[C::A_BYTES];
-    __shared__ __attribute__((aligned(16))) unsigned char a1[C::A_BYTES];
-    __shared__ __attribute__((aligned(16))) unsigned char b0[C::B_BYTES];
-    __shared__ __attribute__((aligned(16))) unsigned char b1[C::B_BYTES];
+    static_assert(ST == 2 || (ST <= 4 && 2 * C::PER_STAGE < 16), "stage count / vmcnt range");
+    __shared__ __attribute__((aligned(16))) unsigned char abuf[ST][C::A_BYTES];
+    __shared__ __attribute__((aligned(16))) unsigned char bbuf[ST][C::B_BYTES];
+    unsigned char *const a0 = abuf[0], *const a1 = abuf[1];
+    unsigned char *const b0 = bbuf[0], *const b1 = bbuf[1];
 
     const GArgs &a = args;
     const int tid = threadIdx.x;
@@ -227,23 +236,49 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
     };
 
     const int n_kt = a.K / BK;
-    dma(0, a0, b0);
-    wait_dma_all();
-    __syncthreads();
-    int kt = 0;
-    for (; kt + 1 < n_kt; kt += 2) {
-        dma(kt + 1, a1, b1);
-        compute(a0, b0);
+    if constexpr (ST == 2) {
+        dma(0, a0, b0);
         wait_dma_all();
         __syncthreads();
-        if (kt + 2 < n_kt)
-            dma(kt + 2, a0, b0);
-        compute(a1, b1);
-        wait_dma_all();
-        __syncthreads();
+        int kt = 0;
+        for (; kt + 1 < n_kt; kt += 2) {
+            dma(kt + 1, a1, b1);
+            compute(a0, b0);
+            wait_dma_all();
+            __syncthreads();
+            if (kt + 2 < n_kt)
+                dma(kt + 2, a0, b0);
+            compute(a1, b1);
+            wait_dma_all();
+            __syncthreads();
+        }
+        if (kt < n_kt)
+            compute(a0, b0);
+    } else {
+        // ring: K step kt lives in stage kt % ST.  Before step kt, wait for
+        // its loads (those of the up to ST - 2 later steps already issued
+        // may stay in flight), then one barrier: every thread's part of
+        // step kt is in LDS and every wave is done with step kt - 1, whose
+        // stage takes step kt + ST - 1.
+#pragma unroll
+        for (int st = 0; st < ST - 1; ++st)
+            if (st < n_kt)
+                dma(st, abuf[st], bbuf[st]);
+        for (int kt = 0; kt < n_kt; ++kt) {
+            const int ahead = min(ST - 2, n_kt - 1 - kt);
+            if (ahead >= 2)
+                wait_dma_upto<2 * C::PER_STAGE>();
+            else if (ahead == 1)
+                wait_dma_upto<C::PER_STAGE>();
+            else
+                wait_dma_all();
+            __syncthreads();
+            const int nx = kt + ST - 1;
+            if (nx < n_kt)
+                dma(nx, abuf[nx % ST], bbuf[nx % ST]);
+            compute(abuf[kt % ST], bbuf[kt % ST]);
+        }
     }
-    if (kt < n_kt)
-        compute(a0, b0);
 
     // epilogue: lane holds column wn + 32j + col, rows wm + 32i + 8(r/4) +
     // 4half + r%4 of the tile
@@ -416,15 +451,15 @@ bool overlaps(const void *p, size_t pn, const void *q, size_t qn)
     return x < y + qn && y < x + pn;
 }
 
-template <int BM, int BN>
+template <int BM, int BN, int ST>
 hipError_t launch(GArgs &a, bool c_bf16, hipStream_t s)
 {
     a.tiles_n = a.N / BN;
     a.n_wg = (a.M / BM) * a.tiles_n;
     if (c_bf16)
-        hipLaunchKernelGGL((gemm_kernel<BM, BN, true>), dim3(a.n_wg), dim3(NT), 0, s, a);
+        hipLaunchKernelGGL((gemm_kernel<BM, BN, ST, true>), dim3(a.n_wg), dim3(NT), 0, s, a);
     else
-        hipLaunchKernelGGL((gemm_kernel<BM, BN, false>), dim3(a.n_wg), dim3(NT), 0, s, a);
+        hipLaunchKernelGGL((gemm_kernel<BM, BN, ST, false>), dim3(a.n_wg), dim3(NT), 0, s, a);
     return hipGetLastError();
 }
 
@@ -466,9 +501,13 @@ ta_status gemm_bf16(const void *A, const void *B, void *C, int c_bf16, int M, in
         return e == hipSuccess ? TA_OK : TA_ERR_LAUNCH;
     }
     // 256 x 256 tiles when they give at least one workgroup per CU
+    // (a ring of four 128 x 128 stages when even those give at most one
+    // workgroup per CU)
     const bool big = M % 256 == 0 && N % 256 == 0 && (int64_t)(M / 256) * (N / 256) >= 256;
-    const hipError_t e = big ? launch<256, 256>(a, c_bf16 != 0, s)
-                             : launch<128, 128>(a, c_bf16 != 0, s);
+    const bool ring = (int64_t)(M / 128) * (N / 128) <= 256;
+    const hipError_t e = big    ? launch<256, 256, 2>(a, c_bf16 != 0, s)
+                         : ring ? launch<128, 128, 4>(a, c_bf16 != 0, s)
+                                : launch<128, 128, 2>(a, c_bf16 != 0, s);
     return e == hipSuccess ? TA_OK : TA_ERR_LAUNCH;
 }
 

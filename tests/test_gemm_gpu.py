@@ -42,7 +42,11 @@ def check(tag, c, a, b, rows=None, bf16=False):
     assert worst <= 1.0, tag
 
 
-SHAPES = [(128, 128, 64), (256, 256, 64), (256, 384, 192), (512, 768, 320), (384, 128, 1024)]
+# at most 256 tiles of 128 x 128 (all but the last): the four-stage ring,
+# with K steps 1, 3 (= stages in flight), 5 and 16; the last one has more
+# tiles, but too few of 256 x 256: double-buffered 128 x 128 tiles
+SHAPES = [(128, 128, 64), (256, 256, 64), (256, 384, 192), (512, 768, 320), (384, 128, 1024),
+          (2304, 2304, 128)]
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=[str(s) for s in SHAPES])
@@ -56,10 +60,10 @@ def test_gemm_full_compare(ta, shape):
     check(f"gemm {shape}", c, a, b)
 
 
-@pytest.mark.parametrize("name", ["gemm_m0", "gemm_m5", "gemm_m3"])
+@pytest.mark.parametrize("name", ["gemm_m0", "gemm_m4", "gemm_m5", "gemm_m3"])
 def test_gemm_workload_sampled(ta, name):
-    """The paper's shapes at full size (both tile configurations): sampled
-    rows against the oracle, every element finite."""
+    """The paper's shapes at full size (all three tile configurations):
+    sampled rows against the oracle, every element finite."""
     w = gen.GEMM_WORKLOADS[name]
     print(f"gemm workload {name} {w.describe()}", flush=True)
     a, b = gen.make_gemm_inputs(w, seed=0)
