@@ -106,9 +106,13 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p)
 __device__ __forceinline__ int a_swz(int r) { return (r >> 1) & 7; }
 __device__ __forceinline__ int b_swz(int r) { return 4 * (r & 3); }
 
-template <int BM, int BN>
+// KS = 1: the eight waves tile C as 2 x 4; KS = 2: as 1 x 4, twice, the two
+// groups of four taking the two halves of every K step (each wave then reads
+// half as much of the B tile per flop through the transpose read), their
+// sums added in LDS at the end
+template <int BM, int BN, int KS = 1>
 struct Cfg {
-    static constexpr int WM = BM / 2, WN = BN / 4;        // wave tile (2 x 4 waves)
+    static constexpr int WM = KS == 2 ? BM : BM / 2, WN = BN / 4;   // wave tile
     static constexpr int FM = WM / 32, FN = WN / 32;      // 32 x 32 blocks per wave
     static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BK * BN * 2;
     static constexpr int A_PER_THREAD = BM * (BK / 8) / NT;   // 16-byte slots
@@ -121,10 +125,12 @@ struct Cfg {
 // flight during the MFMAs) or a ring of three or four (ST - 1 tiles in
 // flight) for grids of at most one workgroup per CU, where no other
 // workgroup's MFMAs cover the wait for a tile.
-template <int BM, int BN, int ST, bool CBF16>
+template <int BM, int BN, int ST, int KS, bool CBF16>
 __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
 {
-    using C = Cfg<BM, BN>;
+    using C = Cfg<BM, BN, KS>;
+    static_assert(KS == 1 || (KS == 2 && C::A_BYTES >= 64 * 64 * 4 && C::B_BYTES >= 64 * 64 * 4),
+                  "the K-half sums need four 16 KB stage buffers");
     static_assert(ST == 2 || (ST <= 4 && 2 * C::PER_STAGE < 16), "stage count / vmcnt range");
     __shared__ __attribute__((aligned(16))) unsigned char abuf[ST][C::A_BYTES];
     __shared__ __attribute__((aligned(16))) unsigned char bbuf[ST][C::B_BYTES];
@@ -153,7 +159,8 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
         tn = w / GROUP_M;
     }
     const int m0 = tm * BM, n0 = tn * BN;
-    const int wm = (wave >> 2) * C::WM, wn = (wave & 3) * C::WN;
+    const int wm = KS == 2 ? 0 : (wave >> 2) * C::WM, wn = (wave & 3) * C::WN;
+    const int kg = KS == 2 ? wave_u >> 2 : 0;      // this wave's half of each K step
 
     // per-lane DMA source offsets within a stage's tiles.  A slot
     // i*NT + 64w + l is row s / 8, stored chunk s % 8 (fetched from chunk
@@ -207,7 +214,8 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
 
     auto compute = [&](const unsigned char *as, const unsigned char *bs) {
 #pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
+        for (int kq = 0; kq < BK / 16 / KS; ++kq) {
+            const int ks = kg * (BK / 16 / KS) + kq;
             bf16x8 av[C::FM], bv[C::FN];
 #pragma unroll
             for (int i = 0; i < C::FM; ++i) {
@@ -278,6 +286,29 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
                 dma(nx, abuf[nx % ST], bbuf[nx % ST]);
             compute(abuf[kt % ST], bbuf[kt % ST]);
         }
+    }
+
+    if constexpr (KS == 2) {
+        // the second K half's sums go through LDS (wave 4 + c into stage
+        // buffer c, lane-major) to wave c, which adds them and stores
+        __syncthreads();   // every wave is done with the stage buffers
+        float *red = (float *)((wave & 3) == 0 ? abuf[0] : (wave & 3) == 1 ? abuf[1]
+                               : (wave & 3) == 2 ? bbuf[0] : bbuf[1]);
+        if (kg == 1) {
+#pragma unroll
+            for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    red[(i * 16 + r) * 64 + lane] = acc[i][0][r];
+        }
+        __syncthreads();
+        if (kg == 1)
+            return;
+#pragma unroll
+        for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[i][0][r] += red[(i * 16 + r) * 64 + lane];
     }
 
     // epilogue: lane holds column wn + 32j + col, rows wm + 32i + 8(r/4) +
@@ -451,15 +482,15 @@ bool overlaps(const void *p, size_t pn, const void *q, size_t qn)
     return x < y + qn && y < x + pn;
 }
 
-template <int BM, int BN, int ST>
+template <int BM, int BN, int ST, int KS>
 hipError_t launch(GArgs &a, bool c_bf16, hipStream_t s)
 {
     a.tiles_n = a.N / BN;
     a.n_wg = (a.M / BM) * a.tiles_n;
     if (c_bf16)
-        hipLaunchKernelGGL((gemm_kernel<BM, BN, ST, true>), dim3(a.n_wg), dim3(NT), 0, s, a);
+        hipLaunchKernelGGL((gemm_kernel<BM, BN, ST, KS, true>), dim3(a.n_wg), dim3(NT), 0, s, a);
     else
-        hipLaunchKernelGGL((gemm_kernel<BM, BN, ST, false>), dim3(a.n_wg), dim3(NT), 0, s, a);
+        hipLaunchKernelGGL((gemm_kernel<BM, BN, ST, KS, false>), dim3(a.n_wg), dim3(NT), 0, s, a);
     return hipGetLastError();
 }
 
@@ -501,13 +532,13 @@ ta_status gemm_bf16(const void *A, const void *B, void *C, int c_bf16, int M, in
         return e == hipSuccess ? TA_OK : TA_ERR_LAUNCH;
     }
     // 256 x 256 tiles when they give at least one workgroup per CU
-    // (a ring of four 128 x 128 stages when even those give at most one
-    // workgroup per CU)
+    // (128 x 128 tiles: K steps split over two groups of waves; a ring of
+    // four stages when even these tiles give at most one workgroup per CU)
     const bool big = M % 256 == 0 && N % 256 == 0 && (int64_t)(M / 256) * (N / 256) >= 256;
     const bool ring = (int64_t)(M / 128) * (N / 128) <= 256;
-    const hipError_t e = big    ? launch<256, 256, 2>(a, c_bf16 != 0, s)
-                         : ring ? launch<128, 128, 4>(a, c_bf16 != 0, s)
-                                : launch<128, 128, 2>(a, c_bf16 != 0, s);
+    const hipError_t e = big    ? launch<256, 256, 2, 1>(a, c_bf16 != 0, s)
+                         : ring ? launch<128, 128, 4, 2>(a, c_bf16 != 0, s)
+                                : launch<128, 128, 2, 2>(a, c_bf16 != 0, s);
     return e == hipSuccess ? TA_OK : TA_ERR_LAUNCH;
 }
 
