@@ -13,10 +13,16 @@
 //    per flop and run at a ~6 % higher clock under the board's power limit,
 //    but with one wave per SIMD their matrix cores idle at every barrier and
 //    operand wait: measured 1-3 % slower at 8192^3 and 4096 x 8192 x 8192.
+//    128 x 128 tiles instead split every K step over two groups of four
+//    waves (1 x 4 each) or, with one workgroup per CU, four groups of two
+//    (1 x 2 each), each group covering the whole tile for its share of the
+//    step: fewer operand reads per flop; the groups' sums meet in LDS.
 //  * K advances in steps of 64.  The A tile [BM][64] and the B tile [64][BN]
 //    go global -> LDS by DMA (buffer_load_dwordx4 ... lds, issued as inline
 //    assembly and waited for explicitly), double-buffered: the DMA of step
-//    k+1 runs under the MFMAs of step k.
+//    k+1 runs under the MFMAs of step k.  With one workgroup per CU (small
+//    grids of 128 x 128 tiles) a ring of four stages keeps three steps in
+//    flight instead.
 //  * A operands (32 rows x 8 consecutive k per lane) are ds_read_b128 from
 //    the A tile, 16-byte chunk c of row r stored at c ^ ((r >> 1) & 7).  B
 //    operands (8 consecutive k of one column per lane) come from the
@@ -106,13 +112,14 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p)
 __device__ __forceinline__ int a_swz(int r) { return (r >> 1) & 7; }
 __device__ __forceinline__ int b_swz(int r) { return 4 * (r & 3); }
 
-// KS = 1: the eight waves tile C as 2 x 4; KS = 2: as 1 x 4, twice, the two
-// groups of four taking the two halves of every K step (each wave then reads
-// half as much of the B tile per flop through the transpose read), their
-// sums added in LDS at the end
+// KS = 1: the eight waves tile C as 2 x 4.  KS = 2 or 4: KS groups of 8 / KS
+// waves, each group tiling C as 1 x (8 / KS) for its share of every K step
+// (a wave then reads less of the tiles per flop, most of all of B through
+// the transpose read); the groups' sums are added in LDS at the end.
 template <int BM, int BN, int KS = 1>
 struct Cfg {
-    static constexpr int WM = KS == 2 ? BM : BM / 2, WN = BN / 4;   // wave tile
+    static constexpr int WPG = 8 / KS;                               // waves per group
+    static constexpr int WM = KS == 1 ? BM / 2 : BM, WN = KS == 1 ? BN / 4 : BN / WPG;
     static constexpr int FM = WM / 32, FN = WN / 32;      // 32 x 32 blocks per wave
     static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BK * BN * 2;
     static constexpr int A_PER_THREAD = BM * (BK / 8) / NT;   // 16-byte slots
@@ -129,8 +136,9 @@ template <int BM, int BN, int ST, int KS, bool CBF16>
 __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
 {
     using C = Cfg<BM, BN, KS>;
-    static_assert(KS == 1 || (KS == 2 && C::A_BYTES >= 64 * 64 * 4 && C::B_BYTES >= 64 * 64 * 4),
-                  "the K-half sums need four 16 KB stage buffers");
+    static_assert(KS == 1 || ((KS == 2 || KS == 4) && C::A_BYTES == 16384 &&
+                              C::B_BYTES == 16384 && C::FM * C::FN * 4096 * C::WPG == 65536),
+                  "a group's sums fill the four 16 KB stage buffers");
     static_assert(ST == 2 || (ST <= 4 && 2 * C::PER_STAGE < 16), "stage count / vmcnt range");
     __shared__ __attribute__((aligned(16))) unsigned char abuf[ST][C::A_BYTES];
     __shared__ __attribute__((aligned(16))) unsigned char bbuf[ST][C::B_BYTES];
@@ -159,8 +167,9 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
         tn = w / GROUP_M;
     }
     const int m0 = tm * BM, n0 = tn * BN;
-    const int wm = KS == 2 ? 0 : (wave >> 2) * C::WM, wn = (wave & 3) * C::WN;
-    const int kg = KS == 2 ? wave_u >> 2 : 0;      // this wave's half of each K step
+    const int cw = KS == 1 ? wave & 3 : wave % C::WPG;    // column of the wave's block
+    const int wm = KS == 1 ? (wave >> 2) * C::WM : 0, wn = cw * C::WN;
+    const int kg = KS == 1 ? 0 : wave_u / C::WPG;          // this wave's share of each K step
 
     // per-lane DMA source offsets within a stage's tiles.  A slot
     // i*NT + 64w + l is row s / 8, stored chunk s % 8 (fetched from chunk
@@ -288,27 +297,48 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
         }
     }
 
-    if constexpr (KS == 2) {
-        // the second K half's sums go through LDS (wave 4 + c into stage
-        // buffer c, lane-major) to wave c, which adds them and stores
+    if constexpr (KS > 1) {
+        // group 0 adds the other groups' sums, one group per round, in
+        // group order.  Accumulator block k = i FN + j of the wave in
+        // column cw goes, lane-major, to 4 KB piece k % 4 of stage buffer
+        // cw (FM FN / 4) + k / 4.
+        constexpr int NB = C::FM * C::FN / 4;   // 16 KB buffers per wave
+        auto piece = [&](int k) {
+            const int bi = cw * NB + k / 4;
+            unsigned char *base = bi == 0 ? abuf[0] : bi == 1 ? abuf[1] : bi == 2 ? bbuf[0] : bbuf[1];
+            return (float *)(base + (k % 4) * 4096);
+        };
         __syncthreads();   // every wave is done with the stage buffers
-        float *red = (float *)((wave & 3) == 0 ? abuf[0] : (wave & 3) == 1 ? abuf[1]
-                               : (wave & 3) == 2 ? bbuf[0] : bbuf[1]);
-        if (kg == 1) {
 #pragma unroll
-            for (int i = 0; i < C::FM; ++i)
+        for (int g = 1; g < KS; ++g) {
+            if (kg == g) {
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    red[(i * 16 + r) * 64 + lane] = acc[i][0][r];
+                for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < C::FN; ++j) {
+                        float *p = piece(i * C::FN + j);
+#pragma unroll
+                        for (int r = 0; r < 16; ++r)
+                            p[r * 64 + lane] = acc[i][j][r];
+                    }
+            }
+            __syncthreads();
+            if (kg == 0) {
+#pragma unroll
+                for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < C::FN; ++j) {
+                        const float *p = piece(i * C::FN + j);
+#pragma unroll
+                        for (int r = 0; r < 16; ++r)
+                            acc[i][j][r] += p[r * 64 + lane];
+                    }
+            }
+            if (g + 1 < KS)
+                __syncthreads();   // read before the next group writes
         }
-        __syncthreads();
-        if (kg == 1)
+        if (kg != 0)
             return;
-#pragma unroll
-        for (int i = 0; i < C::FM; ++i)
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                acc[i][0][r] += red[(i * 16 + r) * 64 + lane];
     }
 
     // epilogue: lane holds column wn + 32j + col, rows wm + 32i + 8(r/4) +
@@ -532,12 +562,14 @@ ta_status gemm_bf16(const void *A, const void *B, void *C, int c_bf16, int M, in
         return e == hipSuccess ? TA_OK : TA_ERR_LAUNCH;
     }
     // 256 x 256 tiles when they give at least one workgroup per CU
-    // (128 x 128 tiles: K steps split over two groups of waves; a ring of
-    // four stages when even these tiles give at most one workgroup per CU)
+    // (128 x 128 tiles: with at most one workgroup per CU, a ring of four
+    // stages and K steps split over four groups of two waves (169 registers:
+    // two waves per SIMD); otherwise two stages and two groups of four (at
+    // most 128 registers, so that two workgroups share a CU))
     const bool big = M % 256 == 0 && N % 256 == 0 && (int64_t)(M / 256) * (N / 256) >= 256;
     const bool ring = (int64_t)(M / 128) * (N / 128) <= 256;
     const hipError_t e = big    ? launch<256, 256, 2, 1>(a, c_bf16 != 0, s)
-                         : ring ? launch<128, 128, 4, 2>(a, c_bf16 != 0, s)
+                         : ring ? launch<128, 128, 4, 4>(a, c_bf16 != 0, s)
                                 : launch<128, 128, 2, 2>(a, c_bf16 != 0, s);
     return e == hipSuccess ? TA_OK : TA_ERR_LAUNCH;
 }
