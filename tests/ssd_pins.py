@@ -186,6 +186,72 @@ def pin_chunk_size_invariance(ssd, seed=8):
         _check("chunk-size invariance", y, ys[0])
 
 
+def _flip_signs(rng, bits):
+    """bf16 bit array with the sign of a random half of its entries flipped"""
+    m = rng.random(bits.shape) < 0.5
+    return np.where(m, bits ^ np.uint16(0x8000), bits).astype(np.uint16)
+
+
+def _nonneg_bits(bits):
+    return (np.ascontiguousarray(bits) & np.uint16(0x7FFF)).astype(np.uint16)
+
+
+def pin_scan_abs_scale(ssd, seed=9):
+    """chunk_scan_abs, the scale every chunk-scan tolerance is stated against,
+    is the chunk scan with every term replaced by its magnitude.  Three facts
+    fix it without restating it: (1) on non-negative x, Cm, cb, entering
+    states and D every term already is its magnitude, so it equals the chunk
+    scan itself (the decays exp(a) are positive for any sign of A, so a
+    flipped A is caught here); (2) it bounds |chunk scan| element by element
+    (triangle inequality); (3) it is unchanged when the sign of any input
+    entry flips (a dropped magnitude on any operand is caught here)."""
+    Q, L = 16, 40
+    w, inp = gen.random_ssd_problem(1, L, 4, 2, seed=seed, P=4, N=8, Q=Q)
+    rng = np.random.default_rng(seed)
+    nc = w.nc
+    x, Cm = inp["x"], inp["Cm"]
+    cb = rng.standard_normal((1, nc, 2, Q, Q))
+    Hs = rng.standard_normal((1, nc, 4, 4, 8))
+    D = rng.standard_normal(4)
+    dt, A = inp["dt"], inp["A"]
+    assert (np.asarray(A) < 0).all(), "the pin needs decaying heads"
+    # (1) non-negative operands
+    xp, Cp = _nonneg_bits(x), _nonneg_bits(Cm)
+    _check("scan_abs == scan on non-negative operands",
+           ssd.chunk_scan_abs(xp, Cp, np.abs(cb), dt, A, np.abs(Hs), np.abs(D), Q),
+           ssd.chunk_scan(xp, Cp, np.abs(cb), dt, A, np.abs(Hs), np.abs(D), Q))
+    # (2) triangle inequality on signed operands
+    y = ssd.chunk_scan(x, Cm, cb, dt, A, Hs, D, Q)
+    ya = ssd.chunk_scan_abs(x, Cm, cb, dt, A, Hs, D, Q)
+    slack = 1e-12 * max(1.0, float(np.abs(ya).max()))
+    assert (np.abs(y) <= ya + slack).all(), "|chunk_scan| exceeds chunk_scan_abs"
+    # (3) sign flips of every operand leave it unchanged
+    flip = lambda a: np.where(rng.random(np.shape(a)) < 0.5, -a, a)
+    yf = ssd.chunk_scan_abs(_flip_signs(rng, x), _flip_signs(rng, Cm), flip(cb), dt, A,
+                            flip(Hs), flip(D), Q)
+    _check("scan_abs under sign flips", yf, ya)
+
+
+def pin_state_abs_scale(ssd, seed=10):
+    """chunk_state_abs, the scale of the chunk-state tolerances: equal to the
+    chunk state on non-negative x and Bm, at least |chunk state| on signed
+    ones, and unchanged by sign flips of x and Bm entries"""
+    Q, L = 16, 40
+    _, inp = gen.random_ssd_problem(2, L, 4, 2, seed=seed, P=4, N=8, Q=Q)
+    rng = np.random.default_rng(seed)
+    x, Bm, dt, A = inp["x"], inp["Bm"], inp["dt"], inp["A"]
+    xp, Bp = _nonneg_bits(x), _nonneg_bits(Bm)
+    _check("state_abs == state on non-negative operands",
+           ssd.chunk_state_abs(xp, Bp, dt, A, Q), ssd.chunk_state(xp, Bp, dt, A, Q))
+    s = ssd.chunk_state(x, Bm, dt, A, Q)
+    sa = ssd.chunk_state_abs(x, Bm, dt, A, Q)
+    slack = 1e-12 * max(1.0, float(np.abs(sa).max()))
+    assert (np.abs(s) <= sa + slack).all(), "|chunk_state| exceeds chunk_state_abs"
+    _check("state_abs under sign flips",
+           ssd.chunk_state_abs(_flip_signs(rng, x), _flip_signs(rng, Bm), dt, A, Q), sa)
+
+
 ALL_PINS = [pin_recurrence, pin_quadratic, pin_chunk_state_from_zero,
             pin_no_decay_linear_attention, pin_bmm_brute_force, pin_scan_entering_state_only,
-            pin_scan_linear_in_inputs, pin_chunk_size_invariance]
+            pin_scan_linear_in_inputs, pin_chunk_size_invariance,
+            pin_scan_abs_scale, pin_state_abs_scale]

@@ -42,6 +42,13 @@ MUTANTS = {
                        'return np.einsum("bclgn,bcsgn->bcgsl", Cc, Bc)'),
     "scan_no_skip": ("y = y + np.asarray(D, dtype=np.float64)[None, None, None, :, None] * Xc",
                      "y = y"),
+    # the tolerance scales (chunk_scan_abs / chunk_state_abs)
+    "scan_abs_growth": ("np.asarray(A), np.abs(prev_states)", "np.abs(A), np.abs(prev_states)"),
+    "scan_abs_signed_cb": ("np.abs(cb), dt", "cb, dt"),
+    "scan_abs_signed_states": ("np.asarray(A), np.abs(prev_states)", "np.asarray(A), prev_states"),
+    "scan_abs_signed_skip": ("np.abs(D), Q)", "D, Q)"),
+    "state_abs_signed_x": ("return chunk_state(absbits(x), absbits(Bm), dt, A, Q)",
+                           "return chunk_state(x, absbits(Bm), dt, A, Q)"),
     "widen_truncate": ("return (b.astype(np.uint32) << np.uint32(16))",
                        "return ((b & np.uint16(0xFF00)).astype(np.uint32) << np.uint32(16))"),
 }
