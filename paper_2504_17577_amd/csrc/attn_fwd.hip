@@ -27,9 +27,17 @@
 //    are applied.
 //  * Two workgroups share each CU (two waves per SIMD), so the MFMAs of one
 //    wave overlap the softmax arithmetic of the other.
-//  * The running max is only raised when a row's tile max exceeds it by more
-//    than 2^8 (lazy rescaling): until then weights stay <= 2^8 and the
-//    accumulator needs no rescale.  The final result is the same softmax.
+//  * The running max m is raised (and the accumulator and row sum
+//    rescaled) only when a row's tile max passes the level
+//    m + min(8, max(0, log2(l / 4))), l being the lane's running row sum.
+//    Below that level a new key's weight is at most max(1, l / 4) and 2^8:
+//    a key weighted above 1 can end with at most a fifth of its row's mass,
+//    so the bf16 rounding of its weight is diluted, while a key that could
+//    dominate its row raises the max first and is weighted exactly 1.  In
+//    exact arithmetic the result is the same softmax for any level; the
+//    level is computed once per tile, off the path from the scores to the
+//    rescale decision, and on rows with many comparable keys it rarely
+//    triggers after the first tiles.
 //  * Causal: key tiles beyond the last visible key of the workgroup are not
 //    visited; only tiles crossing the diagonal or the end of the sequence
 //    take the masked path; there, waves whose queries see none of a tile
@@ -66,7 +74,9 @@ constexpr int NT = 256;      // threads per workgroup
 constexpr int NXCD = 8;      // XCDs per MI355X
 constexpr float LOG2E = 1.44269504088896340736f;
 constexpr float LN2 = 0.69314718055994530942f;
-constexpr float RESCALE_SLACK = 8.0f;   // base-2 headroom before the max is raised
+constexpr float RESCALE_SLACK = 8.0f;   // base-2 headroom: weights never exceed 2^8
+constexpr float RAISE_SHARE_LOG2 = -2.0f;  // log2 of the share (1/4) of l a key may
+                                            // weigh before the max is raised
 // word 3 of a raw (unswizzled, stride 0) buffer resource on CDNA: 32-bit
 // data format, loads past num_records return zero
 [[maybe_unused]] constexpr int BUF_RSRC_WORD3 = 0x00020000;
@@ -158,6 +168,7 @@ struct Kernel {
     bf16x8 qreg[C::KK];
     f32x16 acc_o[C::DB];
     float m_run, l_run;
+    float m_trig;   // the running max is raised when a tile max exceeds this
 
     __device__ Kernel(const Args &args) : a(args) {}
 
@@ -229,8 +240,9 @@ struct Kernel {
             }
     }
 
-    // Online softmax, first half: mask, row max, and (rarely) raise the
-    // running max and rescale the accumulator.
+    // Online softmax, first half: mask, row max, and (when some row's tile
+    // max passes its level m_trig) raise the running max and rescale the
+    // accumulator.
     template <bool MASKED>
     __device__ __forceinline__ void row_max(int j, f32x16 (&s)[2])
     {
@@ -249,8 +261,10 @@ struct Kernel {
             }
         mx = max_halves(mx);
         const float m_tile = MASKED && mx == -INFINITY ? -INFINITY : mx * a.c;
-        // raise the running max only past the slack (wave-uniform decision)
-        if (__builtin_amdgcn_ballot_w64(m_tile > m_run + RESCALE_SLACK)) {
+        // raise the running max when some row passes its level (a
+        // wave-uniform decision; every lane of the wave then rescales, by 1
+        // where its own max did not move)
+        if (__builtin_amdgcn_ballot_w64(m_tile > m_trig)) {
             // (the branch is wave-uniform: a lane whose row has seen no key
             // yet may have m_run = m_tile = -inf; its alpha is 1, not NaN)
             const float m_new = fmaxf(m_run, m_tile);
@@ -289,6 +303,10 @@ struct Kernel {
                 pk[b][r >> 1] = pack_bf16(p0, p1);
             }
         l_run += rowsum;
+        // the level for the next tile: m + min(8, max(0, log2(l / 4)));
+        // l = 0 (no key seen yet) gives m itself
+        m_trig = m_run + fminf(RESCALE_SLACK,
+                               fmaxf(0.f, RAISE_SHARE_LOG2 + __builtin_amdgcn_logf(l_run)));
 
         // MFMA k-slot t of half h stands for key 16ks + 4h + t (t < 4) or
         // 16ks + 8 + 4h + t-4, matching where the accumulator layout left P
@@ -422,6 +440,7 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(Args args)
             k.acc_o[db][r] = 0.f;
     k.m_run = -INFINITY;
     k.l_run = 0.f;
+    k.m_trig = -INFINITY;
 
     // wave w sees tile j unless every key in it is beyond its last query
     auto active = [&](int j) {

@@ -10,26 +10,34 @@
 // cache serving again as the value).  The design is this library's own for
 // CDNA4:
 //
-//  * One workgroup of four wave64s (one per SIMD) owns up to 128 query heads
+//  * One workgroup of four wave64s (one per SIMD) owns HB = 64 query heads
 //    of one latent head of one batch element, and one range of cache tiles
-//    (a key split).  Each wave owns 32 heads.  S^T = K Q^T with
-//    v_mfma_f32_32x32x16_bf16: A = 32 cache rows from LDS, B = the 576-wide
-//    query of the wave's heads, held in registers for the whole kernel.  In
-//    the accumulator layout lane l owns head l % 32, so the softmax row
+//    (a key split).  The waves form two pairs, each pair owning 32 heads.
+//    S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (A = 32 cache rows from LDS,
+//    B = the query of the pair's heads, held in registers for the whole
+//    kernel): the two waves of a pair each take half of the 576-wide
+//    contraction (18 of its 36 k-steps) and exchange their partial scores
+//    through LDS, so both hold the full scores of the tile.  In the
+//    accumulator layout lane l owns head l % 32, so the softmax row
 //    reductions are in-lane plus one v_permlane32_swap.
 //  * O^T += V^T P^T: the bf16 weights already sit in the B-operand layout;
 //    V^T comes from the same latent rows in LDS through the transpose read
-//    ds_read_b64_tr_b16.  The 512 x 32 fp32 accumulator takes 256 registers
-//    per lane: the register file (512 KB per CU) holds the per-head state,
-//    LDS only the streamed cache tiles.
+//    ds_read_b64_tr_b16.  Each wave of a pair accumulates half (256) of the
+//    512 output dims of its 32 heads: 128 fp32 registers per lane, kept in
+//    the matrix-core registers; LDS holds only the streamed cache tiles and
+//    the score exchange.
 //  * Cache tiles of 32 positions go global -> LDS by DMA (buffer_load_dwordx4
-//    ... lds), double-buffered: the latent part [32][512] and the rotary part
-//    [32][64] in two regions.  16-byte chunks are XOR-swizzled so that the
+//    ... lds) into a ring of four buffers, three tiles ahead of the one in
+//    use: the latent part [32][512] and the rotary part [32][64] in two
+//    regions.  16-byte chunks are XOR-swizzled so that the
 //    score operand reads (ds_read_b128) and the transpose reads of the same
 //    latent rows are both bank-conflict free (chunk c of latent row r at
 //    c ^ (((r & 3) << 2) | ((r >> 2) & 3)), of rotary row r at c ^ ((r >> 1) & 7)).
-//  * Online softmax as in the attention kernel: running max raised lazily
-//    (slack 2^8), weights rounded to bf16 for the P V product, fp32 sums.
+//  * Online softmax as in the attention kernel: the running max m is raised
+//    when a head's tile max passes m + min(8, max(0, log2(l / 4))) (l the
+//    lane's running sum), so a position that could dominate a head is
+//    weighted exactly 1; weights rounded to bf16 for the P V product, fp32
+//    sums.
 //  * Key splits write per-split (O_s, LSE_s) to a workspace; the merge kernel
 //    of split_combine.h combines them exactly.
 #include <hip/hip_runtime.h>
@@ -68,7 +76,9 @@ constexpr int ROT_PER_THREAD = BN * (DR / 8) / NT;
 constexpr int NXCD = 8;
 constexpr float LOG2E = 1.44269504088896340736f;
 constexpr float LN2 = 0.69314718055994530942f;
-constexpr float RESCALE_SLACK = 8.0f;
+constexpr float RESCALE_SLACK = 8.0f;       // base-2 headroom: weights never exceed 2^8
+constexpr float RAISE_SHARE_LOG2 = -2.0f;   // log2 of the share (1/4) of l a position may
+                                            // weigh before the max is raised
 [[maybe_unused]] constexpr int BUF_RSRC_WORD3 = 0x00020000;
 static_assert(LAT_PER_THREAD == 8 && ROT_PER_THREAD == 1, "tile/thread mismatch");
 
@@ -179,6 +189,7 @@ struct Mla {
     bf16x8 qreg[KKH];               // the query's k-steps 18 k_half .. +18
     f32x16 acc_o[DBV];
     float m_run, l_run;
+    float m_trig;   // the running max is raised when a tile max exceeds this
 
     __device__ Mla(const MArgs &args) : a(args) {}
 
@@ -350,7 +361,7 @@ struct Mla {
         }
         mx = max_halves(mx);
         const float m_tile = mx * a.c;   // every tile holds a valid position
-        if (__builtin_amdgcn_ballot_w64(m_tile > m_run + RESCALE_SLACK)) {
+        if (__builtin_amdgcn_ballot_w64(m_tile > m_trig)) {
             // acc already holds tile j-1, weighted with the old maximum
             const float m_new = fmaxf(m_run, m_tile);
             const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
@@ -381,6 +392,9 @@ struct Mla {
             pk[r >> 1] = pack_bf16(p0, p1);
         }
         l_run += rowsum;
+        // the level for the next tile (l = 0 gives m itself)
+        m_trig = m_run + fminf(RESCALE_SLACK,
+                               fmaxf(0.f, RAISE_SHARE_LOG2 + __builtin_amdgcn_logf(l_run)));
 
         // tile j+1 must have landed (tiles j+2 and j+3 may stay in flight)
         wait_dma_tiles_left(min(2, max(0, j_hi - 1 - (j + 1))));
@@ -528,6 +542,7 @@ __global__ __launch_bounds__(NT, 1) void mla_decode_kernel(MArgs args)
             k.acc_o[db][r] = 0.f;
     k.m_run = -INFINITY;
     k.l_run = 0.f;
+    k.m_trig = -INFINITY;
 
     // prologue: tiles j_lo .. j_lo+2 in flight, wait for the first
     k.dma_tile(j_lo, lat0, rot0);

@@ -85,6 +85,17 @@ def test_workload_full_size_every_element(ta, name):
     print(f"{name}: max|dO|={eo:.3e} at (b, h, i, d)={tuple(int(x) for x in at)}, "
           f"p99.9|dO|={float(np.quantile(do, 0.999)):.3e}, max|dLSE|={el:.3e}", flush=True)
     assert eo <= O_TOL and el <= LSE_TOL, name
+    # Regression guard, tighter than the target's bound: rounding the softmax
+    # weights to bf16 (relative error <= 2^-8 each, the weight of a row's
+    # dominant key exactly 1) is the kernel's only coarse rounding, and on
+    # these inputs it accounts for max|dO| of about 6e-4 (dense), 4.8e-3 (one
+    # key in 64 scaled by 8, where one or two keys carry most of a row) and
+    # 3.7e-3 (grouped-query causal).  An error beyond these bounds means the
+    # arithmetic changed, e.g. a dominant key whose weight is no longer exact
+    # (which gave 1.5e-2 on the peaky workload).
+    guard = {"dense_d128_s2k": 2e-3, "causal_peaky_d128_s8k": 5e-3,
+             "gqa4_causal_d128_s4k": 5e-3}[name]
+    assert eo <= guard, f"{name}: max|dO| {eo:.3e} above the regression guard {guard:.0e}"
 
 
 def sample_rows(w, rng, n_random):
