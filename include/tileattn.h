@@ -45,7 +45,9 @@ typedef enum {
     TA_ERR_INVALID_SCALE = 5, /* scale is negative, NaN or infinite                         */
     TA_ERR_ALIASING = 6,      /* O or LSE overlaps an input or each other                   */
     TA_ERR_LAUNCH = 7,        /* the HIP runtime reported an error for the launch           */
-    TA_ERR_WORKSPACE = 8      /* attn_fwd_split: workspace NULL or smaller than required    */
+    TA_ERR_WORKSPACE = 8,     /* attn_fwd_split: workspace NULL or smaller than required    */
+    TA_ERR_SCRATCH = 9        /* attn_fwd_split_noalloc: partial results larger than
+                                 TA_SPLIT_SCRATCH_BYTES                                    */
 } ta_status;
 
 /*
@@ -114,6 +116,36 @@ ta_status attn_fwd_split(const void *Q, const void *K, const void *V, void *O, i
                          float *LSE, int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal,
                          float scale, int num_splits, void *workspace, size_t workspace_bytes,
                          void *stream);
+
+/*
+ * attn_fwd_split_noalloc — attn_fwd_split for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, and
+ * harnesses that forbid hipMalloc.  The per-split partial results go to a
+ * static device array inside the library (TA_SPLIT_SCRATCH_BYTES per GPU,
+ * allocated when the library's code is loaded on that GPU and held until the
+ * process ends) instead of a caller workspace; the call itself allocates and
+ * frees nothing.
+ *
+ *   arguments, results and status codes as attn_fwd_split without the
+ *   workspace; TA_ERR_SCRATCH (before any HIP call) if the partial results,
+ *   num_splits' * B*Hq*Sq * (D + 1) * 4 bytes for the num_splits' splits
+ *   actually launched, exceed TA_SPLIT_SCRATCH_BYTES; num_splits == 1 runs
+ *   attn_fwd / attn_fwd_bf16out and touches no scratch.
+ *   TA_ERR_LAUNCH also if the runtime cannot report the current device or
+ *   the scratch's address on it (looked up once per device, on the first
+ *   call there, with that device current).
+ *
+ * Every call on one GPU uses that GPU's one scratch array: calls whose work
+ * overlaps on one GPU (different streams, or different host threads without
+ * ordering) race on it and give wrong results.  Calls ordered on one stream
+ * are safe.  The scratch keeps the last call's contents; nothing in it needs
+ * clearing, since every launched split writes all of its partial rows before
+ * the merge reads them.
+ */
+#define TA_SPLIT_SCRATCH_BYTES (64ull << 20)
+ta_status attn_fwd_split_noalloc(const void *Q, const void *K, const void *V, void *O,
+                                 int o_bf16, float *LSE, int B, int Hq, int Hkv, int Sq, int Sk,
+                                 int D, int causal, float scale, int num_splits, void *stream);
 
 /* Workspace bytes attn_fwd_split needs: num_splits * B*Hq*Sq * (D + 1) * 4
  * for num_splits > 1 (fp32 partial O and LSE per split), 0 for 1.

@@ -52,6 +52,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "tileattn.h"
 #include "split_combine.h"
 
@@ -605,7 +607,8 @@ size_t split_workspace_bytes(int B, int Hq, int Sq, int D, int num_splits)
 // results into the workspace and merges them with combine_kernel.
 ta_status attn_fwd_any(const void *Q, const void *K, const void *V, void *O, bool o_bf16,
                        float *LSE, int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal,
-                       float scale, int num_splits, void *ws, size_t ws_bytes, void *stream)
+                       float scale, int num_splits, void *ws, size_t ws_bytes, void *stream,
+                       bool validate_only = false)
 {
     if (!Q || !K || !V || !O || !LSE)
         return TA_ERR_NULL_POINTER;
@@ -640,6 +643,8 @@ ta_status attn_fwd_any(const void *Q, const void *K, const void *V, void *O, boo
         overlaps(O, o_bytes, LSE, l_bytes))
         return TA_ERR_ALIASING;
     const size_t need = n_split > 1 ? split_workspace_bytes(B, Hq, Sq, D, n_split) : 0;
+    if (validate_only)
+        return TA_OK;
     if (n_split > 1) {
         if (!ws || ws_bytes < need)
             return TA_ERR_WORKSPACE;
@@ -705,6 +710,42 @@ ta_status attn_fwd_any(const void *Q, const void *K, const void *V, void *O, boo
     return e == hipSuccess ? TA_OK : TA_ERR_LAUNCH;
 }
 
+// Per-device address of `tileattn_split_scratch` (declared below, outside
+// this namespace), looked up once per device with that device current.
+constexpr int MAX_DEVICES = 64;
+std::atomic<void *> scratch_addr[MAX_DEVICES];
+
+}  // namespace
+
+// Partial results of attn_fwd_split_noalloc: a file-scope device array
+// instead of a caller workspace, for callers that cannot allocate.  Each GPU
+// the library runs on holds its own copy until the process ends.  In host
+// code the name stands for a host-side shadow, never a device address: host
+// code uses the address hipGetSymbolAddress returns for the current device.
+// The array has external linkage: the runtime finds it by name among the
+// global symbols of the device code object, and a `static` array is a local
+// symbol there (the lookup then aborts the process).
+__device__ __align__(256) unsigned char tileattn_split_scratch[TA_SPLIT_SCRATCH_BYTES];
+
+namespace {
+
+// The device address of `tileattn_split_scratch` on the current device
+// (TA_ERR_LAUNCH if the runtime cannot report the device or the address).
+ta_status scratch_on_current_device(void **out)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES)
+        return TA_ERR_LAUNCH;
+    void *p = scratch_addr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(tileattn_split_scratch)) != hipSuccess || !p)
+            return TA_ERR_LAUNCH;
+        scratch_addr[dev].store(p, std::memory_order_release);
+    }
+    *out = p;
+    return TA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -731,6 +772,30 @@ ta_status attn_fwd_split(const void *Q, const void *K, const void *V, void *O, i
 {
     return attn_fwd_any(Q, K, V, O, o_bf16 != 0, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale,
                         num_splits, workspace, workspace_bytes, stream);
+}
+
+ta_status attn_fwd_split_noalloc(const void *Q, const void *K, const void *V, void *O,
+                                 int o_bf16, float *LSE, int B, int Hq, int Hkv, int Sq, int Sk,
+                                 int D, int causal, float scale, int num_splits, void *stream)
+{
+    // every argument check first, then the size check, then HIP calls
+    ta_status st = attn_fwd_any(Q, K, V, O, o_bf16 != 0, LSE, B, Hq, Hkv, Sq, Sk, D, causal,
+                                scale, num_splits, nullptr, 0, stream, true);
+    if (st != TA_OK)
+        return st;
+    int split_tiles, n_split;
+    split_shape(Sk, num_splits, &split_tiles, &n_split);
+    if (n_split == 1)
+        return attn_fwd_any(Q, K, V, O, o_bf16 != 0, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale,
+                            1, nullptr, 0, stream);
+    if (split_workspace_bytes(B, Hq, Sq, D, n_split) > TA_SPLIT_SCRATCH_BYTES)
+        return TA_ERR_SCRATCH;
+    void *ws = nullptr;
+    st = scratch_on_current_device(&ws);
+    if (st != TA_OK)
+        return st;
+    return attn_fwd_any(Q, K, V, O, o_bf16 != 0, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale,
+                        num_splits, ws, TA_SPLIT_SCRATCH_BYTES, stream);
 }
 
 ta_status ta_split_workspace_bytes(int B, int Hq, int Sq, int D, int num_splits, size_t *bytes)
@@ -805,10 +870,11 @@ const char *ta_status_string(ta_status s)
     case TA_ERR_ALIASING: return "output overlaps an input or the other output";
     case TA_ERR_LAUNCH: return "HIP launch error";
     case TA_ERR_WORKSPACE: return "split workspace missing or too small";
+    case TA_ERR_SCRATCH: return "partial results exceed the static split scratch";
     }
     return "unknown status";
 }
 
-int ta_version(void) { return 300; }
+int ta_version(void) { return 400; }
 
 }  // extern "C"

@@ -17,7 +17,7 @@ TA_OK = 0
 STATUS = {
     0: "TA_OK", 1: "TA_ERR_NULL_POINTER", 2: "TA_ERR_INVALID_SHAPE", 3: "TA_ERR_UNSUPPORTED",
     4: "TA_ERR_MISALIGNED", 5: "TA_ERR_INVALID_SCALE", 6: "TA_ERR_ALIASING", 7: "TA_ERR_LAUNCH",
-    8: "TA_ERR_WORKSPACE",
+    8: "TA_ERR_WORKSPACE", 9: "TA_ERR_SCRATCH",
 }
 
 _lib = None
@@ -46,6 +46,9 @@ def lib():
     L.attn_fwd_split.restype = i
     L.attn_fwd_split.argtypes = [p, p, p, p, i, p, i, i, i, i, i, i, i, ctypes.c_float, i, p,
                                  ctypes.c_size_t, p]
+    L.attn_fwd_split_noalloc.restype = i
+    L.attn_fwd_split_noalloc.argtypes = [p, p, p, p, i, p, i, i, i, i, i, i, i, ctypes.c_float,
+                                         i, p]
     L.ta_split_workspace_bytes.restype = i
     L.ta_split_workspace_bytes.argtypes = [i, i, i, i, i, ctypes.POINTER(ctypes.c_size_t)]
     L.ta_split_heuristic.restype = i
@@ -126,6 +129,13 @@ def attn_fwd_split_raw(Q, K, V, O, o_bf16, LSE, B, Hq, Hkv, Sq, Sk, D, causal, s
     return lib().attn_fwd_split(Q, K, V, O, int(bool(o_bf16)), LSE, B, Hq, Hkv, Sq, Sk, D,
                                 int(causal), float(scale), int(num_splits), workspace,
                                 int(workspace_bytes), stream)
+
+
+def attn_fwd_split_noalloc_raw(Q, K, V, O, o_bf16, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale,
+                               num_splits, stream) -> int:
+    """attn_fwd_split_noalloc with integer pointers; returns the status code."""
+    return lib().attn_fwd_split_noalloc(Q, K, V, O, int(bool(o_bf16)), LSE, B, Hq, Hkv, Sq, Sk, D,
+                                        int(causal), float(scale), int(num_splits), stream)
 
 
 def attn_fwd_raw(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale, stream) -> int:
@@ -237,6 +247,29 @@ def attn_fwd_split(q, k, v, causal: bool = False, scale: float | None = None,
     def raw(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale, stream):
         return attn_fwd_split_raw(Q, K, V, O, o_dtype == torch.bfloat16, LSE, B, Hq, Hkv, Sq, Sk,
                                   D, causal, scale, num_splits, ws_ptr, ws_bytes, stream)
+
+    return _attn(q, k, v, causal, scale, out, lse, stream, o_dtype, raw)
+
+
+def attn_fwd_split_noalloc(q, k, v, causal: bool = False, scale: float | None = None,
+                           num_splits: int | None = None, out=None, lse=None, out_dtype=None,
+                           stream=None):
+    """attn_fwd_split with the partial results in the library's static
+    per-GPU scratch instead of a workspace (the C call allocates nothing;
+    pass ``out`` and ``lse`` to allocate nothing here either).  Calls that
+    overlap on one GPU race on that scratch."""
+    import torch
+
+    o_dtype = torch.float32 if out_dtype is None else out_dtype
+    if o_dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("out_dtype must be torch.float32 or torch.bfloat16")
+    if num_splits is None:
+        B, Hq, Sq, D = q.shape
+        num_splits = ta_split_heuristic(B, Hq, k.shape[1], Sq, k.shape[2], D, causal)
+
+    def raw(Q, K, V, O, LSE, B, Hq, Hkv, Sq, Sk, D, causal, scale, stream):
+        return attn_fwd_split_noalloc_raw(Q, K, V, O, o_dtype == torch.bfloat16, LSE, B, Hq, Hkv,
+                                          Sq, Sk, D, causal, scale, num_splits, stream)
 
     return _attn(q, k, v, causal, scale, out, lse, stream, o_dtype, raw)
 

@@ -29,8 +29,8 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_strings():
-    assert ta.ta_version() >= 300
-    for s in range(9):
+    assert ta.ta_version() >= 400
+    for s in range(10):
         assert ta.ta_status_string(s)
     assert ta.ta_status_string(99) == "unknown status"
     assert ta.ta_tile_shape(64) == ta.ta_tile_shape(128)
@@ -128,6 +128,24 @@ def test_split_validation_before_any_hip_call(change, status):
     rc = ta.attn_fwd_split_raw(a["Q"], a["K"], a["V"], a["O"], a["o_bf16"], a["LSE"], a["B"],
                                a["Hq"], a["Hkv"], a["Sq"], a["Sk"], a["D"], a["causal"],
                                a["scale"], a["splits"], a["ws"], a["ws_bytes"], a["stream"])
+    assert rc == status, f"{change}: got {ta.STATUS.get(rc, rc)}, want {ta.STATUS[status]}"
+
+
+BAD_NOALLOC = [(c, st) for c, st in BAD] + [
+    (dict(splits=0), 2), (dict(splits=129), 2), (dict(splits=-1), 2),
+    # partial results beyond the static scratch: 2 splits of 32 heads x 4096
+    # rows x 129 floats = 135 MB
+    (dict(Hq=32, Hkv=32, Sq=4096, Sk=4096, D=128), 9),
+]
+
+
+@no_gpu
+@pytest.mark.parametrize("change,status", BAD_NOALLOC, ids=[str(c) for c, _ in BAD_NOALLOC])
+def test_split_noalloc_validation_before_any_hip_call(change, status):
+    a = dict(WS_OK, **change)
+    rc = ta.attn_fwd_split_noalloc_raw(a["Q"], a["K"], a["V"], a["O"], a["o_bf16"], a["LSE"],
+                                       a["B"], a["Hq"], a["Hkv"], a["Sq"], a["Sk"], a["D"],
+                                       a["causal"], a["scale"], a["splits"], a["stream"])
     assert rc == status, f"{change}: got {ta.STATUS.get(rc, rc)}, want {ta.STATUS[status]}"
 
 
