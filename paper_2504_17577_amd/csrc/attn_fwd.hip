@@ -671,7 +671,9 @@ ta_status attn_fwd_any(const void *Q, const void *K, const void *V, void *O, boo
     a.split_tiles = split_tiles;
     a.n_wg = (int)n_wg;
     a.c = scale * LOG2E;
-    float *Op = (float *)ws, *Lp = Op + (size_t)n_split * nq;
+    // split partial results: O then LSE of every split (no workspace for one split)
+    float *Op = (float *)ws;
+    float *Lp = n_split > 1 ? Op + (size_t)n_split * nq : nullptr;
     if (n_split > 1) {
         a.O = Op;
         a.LSE = Lp;

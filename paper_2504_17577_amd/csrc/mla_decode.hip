@@ -681,7 +681,9 @@ ta_status mla_decode(const void *Q, const void *Q_pe, const void *KV, const void
     a.split_tiles = split_tiles;
     a.n_wg = (int)n_wg;
     a.c = scale * LOG2E;
-    float *Op = (float *)workspace, *Lp = Op + (size_t)n_split * nq;
+    // split partial results: O then LSE of every split (no workspace for one split)
+    float *Op = (float *)workspace;
+    float *Lp = n_split > 1 ? Op + (size_t)n_split * nq : nullptr;
     if (n_split > 1) {
         a.O = Op;
         a.LSE = Lp;
