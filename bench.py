@@ -13,6 +13,10 @@ oracle.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--out f32|bf16]
                   [--splits 1|N|auto] [--no-cpu-baseline]
+  python bench.py --oracle-all-configs
+                                    # the fp64 oracle on every element of the five
+                                    # target configurations, timed per configuration
+                                    # (and compared with the GPU output if present)
   python bench.py --copy-probe      # plain device copy of known size, for
                                     # scaling rocprofv3 FETCH_SIZE/WRITE_SIZE
   python bench.py --workload gemm_m5 [--out f32|bf16]
@@ -62,18 +66,62 @@ def kernel_digest() -> str:
         return hashlib.blake2b(f.read(), digest_size=8).hexdigest()
 
 
-def read_traffic(workload: str):
-    """HBM bytes per launch from the committed rocprofv3 --pmc summary, or
-    None when there is none or the kernel source changed since."""
-    path = os.path.join(PROFILES, f"attn_fwd_{workload}_traffic.md")
+def _profile_fields(workload: str, kind: str):
+    """The machine-readable ``key: value`` lines of a committed rocprofv3
+    summary (profiles/attn_fwd_<workload>_<kind>.md), or None when there is
+    none or the kernel source changed since it was taken."""
+    path = os.path.join(PROFILES, f"attn_fwd_{workload}_{kind}.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
-    m_src = re.search(r"kernel_source_blake2b:\s*([0-9a-f]+)", text)
-    m_tr = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    if not m_src or not m_tr or m_src.group(1) != kernel_digest():
+    m_src = re.search(r"^kernel_source_blake2b:\s*([0-9a-f]+)", text, re.M)
+    if not m_src or m_src.group(1) != kernel_digest():
         return None
-    return float(m_tr.group(1))
+    return {k: float(v) for k, v in
+            re.findall(r"^([a-z][a-z0-9_]*):\s*([-0-9.eE+]+)\s*$", text, re.M)}
+
+
+def read_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 --pmc FETCH_SIZE /
+    WRITE_SIZE summary (scaled by the copy probe), or None."""
+    f = _profile_fields(workload, "traffic")
+    return None if f is None or "hbm_bytes_per_launch" not in f else f["hbm_bytes_per_launch"]
+
+
+def read_counters(workload: str, ms: float):
+    """MFMA busy fraction, LDS bank-conflict cycles and measured HBM GB/s of
+    the kernel, from the committed SQ-counter and traffic summaries of the
+    same kernel source (rocprofv3 --pmc runs of this command), or None."""
+    f = _profile_fields(workload, "counters")
+    if f is None:
+        return None
+    out = {"source": f"profiles/attn_fwd_{workload}_counters.md"}
+    for key in ("mfma_busy_pct", "lds_bank_conflict_cycles_per_launch", "shader_clock_ghz",
+                "valu_insts_per_mfma"):
+        if key in f:
+            out[key] = f[key]
+    traffic = read_traffic(workload)
+    if traffic is not None:
+        out["hbm_gbs_measured"] = round(traffic / (ms * 1e-3) / 1e9, 1)
+    return out
+
+
+def host_cores() -> int:
+    """Cores this process may run on (its affinity mask)."""
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
+
+
+def blas_threads() -> int:
+    """Threads of numpy's BLAS pool (the numpy oracles' matmuls run there)."""
+    try:
+        from threadpoolctl import threadpool_info
+        n = [p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"]
+        return max(n) if n else 1
+    except Exception:
+        return 1
 
 
 def to_device(a, torch):
@@ -106,6 +154,7 @@ def cpu_baseline(w, q, k, v, budget_s: float = 15.0):
         "value": flops / dt / 1e12,
         "unit": "TFLOP/s",
         "cores": threads,
+        "host_cores": host_cores(),
         "kind": "oracle",
         "sample": f"{n_heads} of {w.B * w.Hq} heads of {w.name} (all {w.Sq} query rows each), "
                   f"fp64 C oracle, {dt:.1f} s wall",
@@ -214,7 +263,8 @@ def mla_cpu_baseline(w, q, q_pe, kv, k_pe, budget_s: float = 15.0):
     ro, rl = oracle.mla_rows(q, q_pe, kv, k_pe, w.scale, rows, nthreads=threads, lib=lib)
     dt = time.perf_counter() - t0
     flops = w.flops() / w.B * n_b
-    info = {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+    info = {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
+            "host_cores": host_cores(), "kind": "oracle",
             "sample": f"{n_b} of {w.B} batch elements of {w.name} (all {w.H} heads each), "
                       f"fp64 C oracle, {dt:.1f} s wall"}
     return info, rows, ro, rl
@@ -405,8 +455,9 @@ def bench_gemm(args, torch, tileattn):
             value, unit = w.flops() * share / dt_s / 1e12, "TFLOP/s"
         result["cpu_baseline"] = {
             "value": value, "unit": unit,
-            "cores": len(os.sched_getaffinity(0)), "kind": "oracle",
-            "sample": f"{n} of {total} {unit_name} of {w.name}, float64 numpy matmul, {dt_s:.1f} s wall"}
+            "cores": blas_threads(), "host_cores": host_cores(), "kind": "oracle",
+            "sample": f"{n} of {total} {unit_name} of {w.name}, float64 numpy matmul "
+                      f"(BLAS threads), {dt_s:.1f} s wall"}
     print(json.dumps(result), flush=True)
 
 
@@ -517,10 +568,51 @@ def bench_ssd(args, torch, tileattn):
         frac = n / (w.B * w.H)
         result["cpu_baseline"] = {
             "value": round(nbytes * frac / dt_s / 1e9, 3), "unit": "GB/s",
-            "cores": len(os.sched_getaffinity(0)), "kind": "oracle",
-            "sample": f"{n} of {w.B * w.H} (batch, head) slices of {w.name}, {op}, numpy float64, "
-                      f"{dt_s:.1f} s wall"}
+            "cores": blas_threads(), "host_cores": host_cores(), "kind": "oracle",
+            "sample": f"{n} of {w.B * w.H} (batch, head) slices of {w.name}, {op}, numpy float64 "
+                      f"(einsum; BLAS threads where it calls BLAS), {dt_s:.1f} s wall"}
     print(json.dumps(result), flush=True)
+
+
+TARGET_WORKLOADS = ("tiny_d64_s128", "causal_d64_s1k", "dense_d128_s2k",
+                    "causal_peaky_d128_s8k", "gqa4_causal_d128_s4k")
+
+
+def oracle_all_configs(args):
+    """The fp64 oracle timed on every output element of the five target
+    configurations (no sampling), each on this host's cores; with a GPU the
+    attention kernel's output is compared with it element by element.  One
+    JSON line per configuration."""
+    import oracle
+
+    torch = None
+    try:
+        import torch as _t
+        if _t.cuda.is_available():
+            torch = _t
+            from paper_2504_17577_amd import tileattn
+    except ImportError:
+        pass
+    threads = oracle.default_threads()
+    lib = oracle.load()
+    for name in TARGET_WORKLOADS:
+        w = gen.WORKLOADS[name]
+        q, k, v = gen.make_inputs(w, seed=args.seed)
+        t0 = time.perf_counter()
+        ro, rl = oracle.attn_fwd(q, k, v, w.causal, w.scale, nthreads=threads, lib=lib)
+        dt = time.perf_counter() - t0
+        line = {"workload": name, "shape": w.describe(), "flops": w.flops(),
+                "oracle_s": round(dt, 3), "oracle_gflops_fp64": round(w.flops() / dt / 1e9, 2),
+                "cores": threads, "host_cores": host_cores(), "elements_compared": None}
+        if torch is not None:
+            o, lse = tileattn.attn_fwd(to_device(q, torch), to_device(k, torch),
+                                       to_device(v, torch), causal=w.causal, scale=w.scale)
+            torch.cuda.synchronize()
+            eo = float(np.abs(o.cpu().numpy() - ro).max())
+            el = float(np.abs(lse.cpu().numpy() - rl).max())
+            line.update({"max_abs_dO": eo, "max_abs_dLSE": el, "elements_compared": int(ro.size),
+                         "within_tolerance": bool(eo <= 2e-2 and el <= 1e-3)})
+        print(json.dumps(line), flush=True)
 
 
 def main():
@@ -542,6 +634,9 @@ def main():
                          "(attn_fwd_split with ta_split_heuristic; workspace allocated "
                          "before the timed region)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--oracle-all-configs", action="store_true",
+                    help="time the fp64 oracle on every element of the five target "
+                         "configurations (and compare the GPU output where there is one)")
     ap.add_argument("--copy-probe", action="store_true")
     ap.add_argument("--sustain", type=float, default=0.0,
                     help="also run the step back to back for this many seconds while "
@@ -555,6 +650,10 @@ def main():
         print(f"bench.py runs on one GPU only: the attention forward here has no multi-GPU "
               f"path (asked for --gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
+
+    if args.oracle_all_configs:
+        oracle_all_configs(args)
+        return
 
     import torch
 
@@ -605,18 +704,25 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # timed region: K launches on this stream between two HIP events
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
+    # timed region: K launches on this stream between two HIP events, with
+    # events between five equal sub-batches as well (recorded on the stream,
+    # no synchronisation inside the region): the board's power management
+    # lowers the clock for the first tens of launches after idle, and the
+    # sub-batch times show where the timed region sat on that curve
+    n_b = 5 if args.steps >= 5 else 1
+    cuts = [round(i * args.steps / n_b) for i in range(n_b + 1)]
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(n_b + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    start.record(stream)
-    for _ in range(args.steps):
-        step()
-    end.record(stream)
+    evs[0].record(stream)
+    for i in range(n_b):
+        for _ in range(cuts[i + 1] - cuts[i]):
+            step()
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms = start.elapsed_time(end) / args.steps
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    batch_ms = [evs[i].elapsed_time(evs[i + 1]) / (cuts[i + 1] - cuts[i]) for i in range(n_b)]
     tflops = w.flops() / (ms * 1e-3) / 1e12
 
     traffic = None if (o_bf16 or n_split > 1) else read_traffic(w.name)
@@ -650,7 +756,12 @@ def main():
             "hbm_gbs_algorithmic": round(w.bytes(2 if o_bf16 else 4) / (ms * 1e-3) / 1e9, 1),
         },
         "wall_s_timed": round(wall, 4),
+        "timed_sub_batches": {"launches": [cuts[i + 1] - cuts[i] for i in range(n_b)],
+                              "ms_per_launch": [round(x, 5) for x in batch_ms],
+                              "median_ms": round(float(np.median(batch_ms)), 5)},
     }
+    counters = None if (o_bf16 or n_split > 1) else read_counters(w.name, ms)
+    result["counters"] = counters
     if args.sustain > 0:
         with PowerSampler() as sampler:
             result["sustained"] = sustained(torch, step, w.flops(), args.sustain, sampler)
