@@ -20,7 +20,8 @@
 //    transpose read ds_read_b64_tr_b16, so V needs no reshuffle.  The
 //    per-row rescale factor is a per-lane scalar.
 //  * K and V tiles go global -> LDS by direct DMA (buffer_load_dwordx4 ...
-//    lds, 16 bytes per lane), double-buffered: the DMA of tile j+1 is issued
+//    lds, 16 bytes per lane, issued as inline assembly and waited for by
+//    the kernel itself), in two stages: the DMA of tile j+1 is issued
 //    before the math on tile j, with one barrier per tile.  Each lane
 //    fetches the 16-byte chunk that belongs at its LDS slot, which is how
 //    the XOR swizzles that keep the MFMA operand reads bank-conflict free
@@ -44,10 +45,15 @@
 //    skip it.
 //  * Epilogue: the normalised O rows are staged in LDS so that each store
 //    instruction writes whole rows.
-//  * Grid: one workgroup per (batch, head, query tile); the hardware deals
-//    consecutive workgroup ids round-robin to the 8 XCDs, so ids are
-//    remapped to give each XCD a contiguous range of heads (their K/V stay
-//    in that XCD's L2), heaviest causal tiles first.
+//  * Work items are (batch, head, query tile) triples; the hardware deals
+//    consecutive workgroup ids round-robin to the 8 XCDs, so each XCD gets
+//    a contiguous range of heads (their K/V stay in that XCD's L2),
+//    heaviest causal tiles first.  Non-causal grids (and grids that fit on
+//    the chip at once) have one workgroup per item.  Larger causal grids are
+//    persistent, two workgroups per CU, each running its items as one
+//    stream of key tiles: the next item's first K/V tile and its Q are
+//    fetched during the current item's last tile, and the current item's O
+//    stores overlap the next item's first tile.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -55,6 +61,7 @@
 #include <atomic>
 
 #include "tileattn.h"
+#include "lds_dma.h"
 #include "split_combine.h"
 
 namespace {
@@ -111,7 +118,7 @@ struct Args {
     int n_qt;        // query tiles per head
     int n_split;     // key-range splits per query tile
     int split_tiles; // key tiles per split
-    int n_wg;        // total workgroups
+    int n_items;     // work items: B * Hq * n_qt * n_split
     float c;         // scale * log2(e)
 };
 
@@ -141,32 +148,60 @@ __device__ __forceinline__ float sum_halves(float x)
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-__device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
-
-// Workgroup id -> (head index b*Hq+h, query tile, key split).  The hardware
-// hands workgroup i to XCD i % 8; give each XCD a contiguous block of
-// logical ids, ordered head-major so a head's K/V stay in one XCD's L2.
-__device__ __forceinline__ void decode_wg(const Args &a, int bid, int &head, int &qt,
-                                          int &split)
+// Work items are (batch * head, query tile, key split) triples, numbered
+// head-major (heaviest causal query tiles of a head first).  The hardware
+// hands workgroup w to XCD w % 8, and each XCD owns a contiguous range of
+// items, so that a head's K/V stay in that XCD's L2.
+__device__ __forceinline__ int xcd_range_lo(const Args &a, int x)
 {
-    const int per = a.n_wg / NXCD, rem = a.n_wg % NXCD;
-    const int xcd = bid % NXCD, idx = bid / NXCD;
-    const int logical = xcd * per + (xcd < rem ? xcd : rem) + idx;
-    const int per_head = a.n_qt * a.n_split;
-    head = logical / per_head;
-    qt = (logical % per_head) / a.n_split;
-    split = logical % a.n_split;
+    const int per = a.n_items / NXCD, rem = a.n_items % NXCD;
+    return x * per + (x < rem ? x : rem);
 }
 
-template <int D, bool CAUSAL>
+__device__ __forceinline__ int xcd_range_n(const Args &a, int x)
+{
+    return a.n_items / NXCD + (x < a.n_items % NXCD ? 1 : 0);
+}
+
+// Workgroup bid's item of round r (-1 past the end of its XCD's range).
+// The workgroups of an XCD (S of them, slot = bid / 8) take its range in
+// rounds of S items, in alternating direction: round r gives slot s the
+// item r*S + s (even r) or r*S + S-1-s (odd r).  For causal items (heaviest
+// query tiles of a head first) this gives every slot about the same work
+// over each pair of rounds, and all the workgroups of an XCD work on the
+// same one or two heads at a time.  With one workgroup per item (grids that
+// fit at once, key splits) there is a single round.
+__device__ __forceinline__ int static_item(const Args &a, int bid, int grid, int r)
+{
+    const int xcd = bid % NXCD, slot = bid / NXCD;
+    const int S = (grid - xcd + NXCD - 1) / NXCD;
+    const int i = r * S + ((r & 1) ? S - 1 - slot : slot);
+    return i < xcd_range_n(a, xcd) ? xcd_range_lo(a, xcd) + i : -1;
+}
+
+// One work item's coordinates and key-tile range (wave-uniform).
+struct Item {
+    int q0;          // first query row
+    int split;       // key split index
+    int j_lo, j_hi;  // key tiles [j_lo, j_hi) of this item
+    int j_fast;      // tiles before this one need no per-element mask
+    size_t row0;     // (b * Hq + hq) * Sq: first row of the head in Q, O, LSE
+    size_t kv_base;  // (b * Hkv + hk) * Sk * D: the head's K/V slice
+};
+
+template <int D, bool CAUSAL, bool OBF16, bool PERSIST>
 struct Kernel {
     using C = Cfg<D>;
 
     const Args &a;
     int wave, lane, col, half;
-    int qi, off, q_last_wave;
-    const uint16_t *Kg, *Vg;
-    uint32_t koff[C::DMA_PER_THREAD], voff[C::DMA_PER_THREAD];  // byte offsets in a tile
+    int wave_u;              // the wave index, in a scalar register
+    int off;                 // Sk - Sq, the bottom-right causal offset
+    Item cur, nxt;           // the item being computed and the workgroup's next one
+    bool has_next;
+    int qi, q_last_wave;     // this lane's query row; last real row of the wave
+    bool wave_has_rows;
+    uint32_t koff, voff;     // byte offsets of this lane's first K / V chunk in a tile
     bf16x8 qreg[C::KK];
     f32x16 acc_o[C::DB];
     float m_run, l_run;
@@ -174,53 +209,122 @@ struct Kernel {
 
     __device__ Kernel(const Args &args) : a(args) {}
 
-    // Each lane's source byte offset (within a tile) for its 16-byte LDS
-    // slots: slot i*NT + 64w + l holds chunk (pc ^ swizzle(r)) of tile row r.
-    __device__ void init_dma()
+    __device__ __forceinline__ Item describe(int L) const
     {
-        const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-#pragma unroll
-        for (int i = 0; i < C::DMA_PER_THREAD; ++i) {
-            const int slot = i * NT + wave_u * 64 + lane;
-            const int r = slot / C::CH, pc = slot % C::CH;
-            koff[i] = 2 * (r * D + 8 * (pc ^ C::kswz(r)));
-            voff[i] = 2 * (r * D + 8 * (pc ^ C::vswz(r)));
+        const int per_head = PERSIST ? a.n_qt : a.n_qt * a.n_split;
+        const int head = L / per_head;
+        int qt = PERSIST ? L % per_head : (L % per_head) / a.n_split;
+        Item it;
+        it.split = PERSIST ? 0 : L % a.n_split;   // persistent grids have no key splits
+        if (CAUSAL)
+            qt = a.n_qt - 1 - qt;   // heaviest query tiles of a head first
+        const int b = head / a.Hq, hq = head % a.Hq;
+        const int hk = hq / a.group;
+        it.q0 = qt * BM;
+        it.row0 = ((size_t)b * a.Hq + hq) * a.Sq;
+        it.kv_base = ((size_t)b * a.Hkv + hk) * (size_t)a.Sk * D;
+        // key tiles to visit, and the first one needing per-element masks
+        const int n_kv_all = (a.Sk + BN - 1) / BN;
+        int n_kv = n_kv_all;
+        int first_masked = (a.Sk % BN) ? n_kv_all - 1 : n_kv_all;
+        if (CAUSAL) {
+            const int q_last_wg = min(it.q0 + BM, a.Sq) - 1;
+            n_kv = min(n_kv_all, (q_last_wg + off) / BN + 1);
+            first_masked = min(first_masked, max(0, (it.q0 + off + 1) / BN));
+            first_masked = min(first_masked, n_kv);
         }
+        it.j_lo = PERSIST ? 0 : it.split * a.split_tiles;
+        it.j_hi = PERSIST ? n_kv : min(n_kv, it.j_lo + a.split_tiles);
+        it.j_fast = min(first_masked, it.j_hi);
+        return it;
     }
 
-    // DMA the K or V tile of keys j*BN .. j*BN+BN-1 into `buf` with
-    // buffer_load_dwordx4 ... lds.  The buffer resource starts at the tile
-    // and ends at the end of this (batch, head) slice; on the ragged last
-    // tile rows past Sk re-read row Sk-1 (their scores are masked and their
-    // weights zero), so no lane addresses past the slice.
-    template <bool IS_V>
-    __device__ __forceinline__ void dma_tile(int j, unsigned char *buf) const
+    // per-lane values of the current item (the per-wave ones from the wave
+    // index in a scalar register, so that branches on them are uniform)
+    __device__ __forceinline__ void set_rows()
     {
-#if __HIP_DEVICE_COMPILE__   // buffer-resource builtins exist in the device pass only
+        qi = cur.q0 + wave * 32 + col;
+        q_last_wave = min(cur.q0 + wave_u * 32 + 31, a.Sq - 1);
+        wave_has_rows = cur.q0 + wave_u * 32 < a.Sq;
+    }
+
+    __device__ __forceinline__ void reset_state()
+    {
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc_o[db][r] = 0.f;
+        m_run = -INFINITY;
+        l_run = 0.f;
+        m_trig = -INFINITY;
+    }
+
+    // Q of this lane's query of item `it`, as the B operand of S^T = K Q^T.
+    // Rows past Sq (padding of the last query tile) read row Sq-1: their
+    // results are never stored.
+    __device__ __forceinline__ void load_q(const Item &it)
+    {
+        const int r = min(it.q0 + wave * 32 + col, a.Sq - 1);
+        const uint16_t *qp = a.Q + (it.row0 + r) * D + 8 * half;
+#pragma unroll
+        for (int kk = 0; kk < C::KK; ++kk)
+            qreg[kk] = __builtin_bit_cast(bf16x8, *(const u32x4 *)(qp + 16 * kk));
+    }
+
+    // Each lane's source byte offset (within a tile) for its 16-byte LDS
+    // slots: slot i*NT + 64w + l holds chunk (pc ^ swizzle(r)) of tile row r.
+    // Row r = i * RPS + (64w + l) / CH, and both swizzles depend on r only
+    // through (64w + l) / CH, so slot i's offset is that of slot 0 plus
+    // i * NT * 16 bytes (RPS rows).
+    __device__ void init_dma()
+    {
+        wave_u = __builtin_amdgcn_readfirstlane(wave);
+        const int slot = wave_u * 64 + lane;
+        const int r = slot / C::CH, pc = slot % C::CH;
+        koff = 2 * (r * D + 8 * (pc ^ C::kswz(r)));
+        voff = 2 * (r * D + 8 * (pc ^ C::vswz(r)));
+    }
+
+    // DMA the K or V tile of keys j*BN .. j*BN+BN-1 of the head slice at
+    // `base` into LDS at `buf` (buffer_load_dwordx4 ... lds, issued as inline
+    // assembly: the compiler does not track these loads, the kernel waits for
+    // them itself at the end of every tile).  The buffer resource starts at
+    // the tile and ends at the end of the slice; on the ragged last tile rows
+    // past Sk re-read row Sk-1 (their scores are masked and their weights
+    // zero), so no lane addresses past the slice.
+    template <bool IS_V>
+    __device__ __forceinline__ void dma_tile(const uint16_t *base, int j,
+                                             const unsigned char *buf) const
+    {
+        constexpr int RPS = NT * 16 / (2 * D);   // tile rows per slot block
         const uint32_t tile_bytes = BN * D * 2;
-        const uint16_t *tile = (IS_V ? Vg : Kg) + (size_t)j * (BN * D);
+        const uint16_t *tile = base + (size_t)j * (BN * D);
         const uint32_t left = (uint32_t)a.Sk * (D * 2) - (uint32_t)j * tile_bytes;
-        const __amdgpu_buffer_rsrc_t rs =
-            __builtin_amdgcn_make_buffer_rsrc((void *)tile, 0, (int)left, BUF_RSRC_WORD3);
-        const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+        const tileattn_dma::u32x4s rs = tileattn_dma::buffer_rsrc(tile, left);
+        const uint32_t lds0 = tileattn_dma::lds_addr(buf) + wave_u * 64 * 16;
+        const uint32_t o0 = IS_V ? voff : koff;
         if ((j + 1) * BN <= a.Sk) {
 #pragma unroll
             for (int i = 0; i < C::DMA_PER_THREAD; ++i)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    rs, (lds_void *)(buf + (i * NT + wave_u * 64) * 16), 16,
-                    IS_V ? voff[i] : koff[i], 0, 0, 0);
+                tileattn_dma::dma16_soff(lds0 + i * NT * 16, o0, i * NT * 16, rs);
         } else {
             const int last_row = a.Sk - 1 - j * BN;
+            const int r0 = (int)(o0 / (2 * D));
 #pragma unroll
             for (int i = 0; i < C::DMA_PER_THREAD; ++i) {
-                uint32_t o = IS_V ? voff[i] : koff[i];
-                if ((int)(o / (2 * D)) > last_row)
-                    o = last_row * (2 * D) + (o % (2 * D));
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    rs, (lds_void *)(buf + (i * NT + wave_u * 64) * 16), 16, o, 0, 0, 0);
+                const uint32_t o = r0 + i * RPS > last_row
+                                       ? last_row * (2 * D) + o0 % (2 * D)
+                                       : o0 + i * NT * 16;
+                tileattn_dma::dma16(lds0 + i * NT * 16, o, rs);
             }
         }
-#endif
+    }
+
+    __device__ __forceinline__ void dma_kv(size_t kv_base, int j, const unsigned char *stage) const
+    {
+        dma_tile<false>(a.K + kv_base, j, stage);
+        dma_tile<true>(a.V + kv_base, j, stage + C::TILE_BYTES);
     }
 
     // S^T[key][query] of one tile (two 32-key blocks, chains interleaved)
@@ -337,215 +441,285 @@ struct Kernel {
         }
     }
 
-    // Steady-state iteration j (all keys of tile j visible to every real
-    // query): DMA K_{j+1} and V_{j+1} into kn and vn while tile j is
-    // processed from kc and vc.
-    __device__ __forceinline__ void fast_step(int j, int n_kv, const unsigned char *kc,
-                                              unsigned char *kn, const unsigned char *vc,
-                                              unsigned char *vn)
+    // wave w sees tile j unless every key in it is beyond its last query
+    __device__ __forceinline__ bool active(int j) const
     {
-        if (j + 1 < n_kv) {
-            dma_tile<false>(j + 1, kn);
-            dma_tile<true>(j + 1, vn);
-        }
+        return wave_has_rows && (!CAUSAL || j * BN <= q_last_wave + off);
+    }
+
+    // Tile j of the current item from the stage at `sc` (K tile, then V
+    // tile).  First the DMA of the next tile of the workgroup's stream goes
+    // into the other stage `sn`: tile j+1 of this item, or on its last tile
+    // the first tile of the next item.  MASKED = false: the tile is fully
+    // visible to every real query of the item (a wave holding only padding
+    // rows past Sq computes on it and never stores).  MASKED = true: waves
+    // skip the tile if they cannot see any of it.  Every thread takes part
+    // in the DMA and the barrier.
+    template <bool MASKED>
+    __device__ __forceinline__ void tile(int j, const unsigned char *sc, const unsigned char *sn)
+    {
+        const bool last = j + 1 == cur.j_hi;
+        if (!last || has_next)
+            dma_kv(last ? nxt.kv_base : cur.kv_base, last ? nxt.j_lo : j + 1, sn);
+        const bool act = !MASKED || active(j);   // wave-uniform
         f32x16 s[2];
-        scores(kc, s);
-        row_max<false>(j, s);
-        exp_pv<false>(s, vc);
-        wait_dma();
+        if (act)
+            scores(sc, s);
+        if (last && has_next) {
+            // the next item's Q, once this tile's score MFMAs (the last
+            // readers of Q) are issued
+            __builtin_amdgcn_sched_barrier(0);
+            load_q(nxt);
+        }
+        if (act) {
+            row_max<MASKED>(j, s);
+            exp_pv<MASKED>(s, sc + C::TILE_BYTES);
+        }
+        tileattn_dma::wait_vmcnt<0>();
         __syncthreads();
+    }
+
+    // Epilogue of the current item: normalise, store O rows (fp32, or bf16
+    // rounded to nearest even) and LSE.  A row that saw no key of its split
+    // (only possible with key splits) stores the empty partial result:
+    // O = 0, LSE = -inf.
+    //   The rows go through LDS so that every store instruction writes whole
+    // rows (lane (col, half) holds 4 consecutive dims of row col per (db, g):
+    // written directly, each instruction would be 32 pieces of 16 or 8
+    // bytes).  The staging area is the stage of the item's last tile, which
+    // every wave has left behind at that tile's barrier (the other stage
+    // holds the next item's first tile, in flight), or all of LDS in a grid
+    // of one workgroup per item; each wave
+    // stages RP of its 32 rows at a time in its own quarter, 16-byte chunk q
+    // of staged row r at q ^ (r % RCH), and reads back only what it wrote
+    // itself (a wave's LDS accesses complete in order).  A barrier then
+    // keeps the next item's DMA into this stage behind every wave's reads;
+    // the stores complete in the background, during the next item's first
+    // tile.
+    template <bool WHOLE_LDS>
+    __device__ __forceinline__ void epilogue(unsigned char *stage)
+    {
+        const float l = sum_halves(l_run);
+        const bool empty = !(l > 0.f);
+        const float inv = empty ? 0.f : 1.f / l;
+        constexpr int EB = OBF16 ? 2 : 4;               // bytes per output element
+        constexpr int RCH = D * EB / 16;                // 16-byte chunks per row
+        constexpr int RPI = 64 / RCH;                   // rows per read instruction
+        // each wave's quarter of the staging area: of the last tile's stage,
+        // or (WHOLE_LDS: one item per workgroup, no DMA in flight) of all of LDS
+        constexpr int QB = (WHOLE_LDS ? 4 : 2) * C::TILE_BYTES / 4;
+        constexpr int RP = QB / (D * EB) < 32 ? QB / (D * EB) : 32;  // rows per pass
+        constexpr int NP = 32 / RP;                     // passes
+        constexpr int NI = RP / RPI;                    // reads per pass
+        static_assert(RP % RPI == 0 && 32 % RP == 0, "staging shape");
+        unsigned char *const stg = stage + wave * QB;
+        // O elements of this item's first row (the split's partial results
+        // start o_split elements apart; bf16 O is never split)
+        const size_t obase = (OBF16 ? 0 : (size_t)cur.split * a.o_split) + cur.row0 * D;
+        // the lane coordinates as opaque values here, so that the staging
+        // addresses are computed here, once per item, and not kept in
+        // registers (or spilled) across the tile loop
+        int col = this->col, half = this->half, lane = this->lane;
+        asm volatile("" : "+v"(col), "+v"(half), "+v"(lane));
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            if (col / RP == p) {
+                const int r = col % RP;
+#pragma unroll
+                for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int byte = (32 * db + 8 * g + 4 * half) * EB;   // within the row
+                        unsigned char *pp =
+                            stg + r * (D * EB) + (((byte >> 4) ^ (r & (RCH - 1))) * 16) + (byte & 15);
+                        const float x0 = acc_o[db][4 * g + 0] * inv, x1 = acc_o[db][4 * g + 1] * inv;
+                        const float x2 = acc_o[db][4 * g + 2] * inv, x3 = acc_o[db][4 * g + 3] * inv;
+                        if (OBF16)
+                            *(u32x2 *)pp = u32x2{pack_bf16(x0, x1), pack_bf16(x2, x3)};
+                        else
+                            *(float4 *)pp = float4{x0, x1, x2, x3};
+                    }
+            }
+            if (p == 0) {
+                // Q has landed before any store is issued: the compiler's own
+                // wait for Q, at the next item's first scores, then finds no
+                // load of its own pending and cannot end up waiting for that
+                // item's tile DMA, which it does not track (unconditional, so
+                // that it covers every path from the load)
+                tileattn_dma::wait_vmcnt<0>();
+            }
+#pragma unroll
+            for (int it = 0; it < NI; ++it) {
+                const int r = it * RPI + lane / RCH, q = lane % RCH;
+                const u32x4 v = *(const u32x4 *)(stg + r * (D * EB) + ((q ^ (r & (RCH - 1))) * 16));
+                const int qr = cur.q0 + wave * 32 + p * RP + r;
+                if (qr < a.Sq) {
+                    if (OBF16)
+                        *(u32x4 *)((uint16_t *)a.O + obase + (size_t)qr * D + 8 * q) = v;
+                    else
+                        *(u32x4 *)((float *)a.O + obase + (size_t)qr * D + 4 * q) = v;
+                }
+            }
+        }
+        if (qi < a.Sq && half == 0)
+            a.LSE[(size_t)cur.split * a.l_split + cur.row0 + qi] =
+                empty ? -INFINITY : (m_run + log2f(l)) * LN2;
+        if (has_next) {
+            // every wave's staging reads complete before any wave's next DMA
+            // into this stage (the stores need not have completed)
+            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+            __builtin_amdgcn_s_barrier();
+        }
+    }
+
+    // The key tiles of the current item, the first in stage `st` (its DMA
+    // already waited for): those before j_fast in one loop, unrolled by two
+    // so that both stage addresses are fixed for the item, the masked ones
+    // in another.  Returns the stage holding the next item's first tile.
+    __device__ __forceinline__ int run_item(unsigned char *lds, int st)
+    {
+        constexpr int SB = 2 * C::TILE_BYTES;   // bytes per stage
+        unsigned char *sa = lds + st * SB, *sb = lds + (st ^ 1) * SB;
+        int j = cur.j_lo;
+        for (; j + 1 < cur.j_fast; j += 2) {
+            tile<false>(j, sa, sb);
+            tile<false>(j + 1, sb, sa);
+        }
+        if (j < cur.j_fast) {
+            tile<false>(j, sa, sb);
+            unsigned char *const t = sa;
+            sa = sb;
+            sb = t;
+            ++j;
+        }
+        for (; j < cur.j_hi; ++j) {
+            tile<true>(j, sa, sb);
+            unsigned char *const t = sa;
+            sa = sb;
+            sb = t;
+        }
+        if (PERSIST)
+            epilogue<false>(sb);
+        else
+            epilogue<true>(lds);
+        return sa == lds ? 0 : 1;
+    }
+
+    // An item whose key split holds no visible key (key splits only, one
+    // item per workgroup): the empty partial result, LSE = -inf and O = 0,
+    // which the combine step weights by zero.
+    __device__ void empty_result(int tid) const
+    {
+        const int r = cur.q0 + tid / 2;
+        if (tid < 2 * BM && r < a.Sq) {
+            float *op = (float *)a.O + (size_t)cur.split * a.o_split + (cur.row0 + r) * D;
+#pragma unroll
+            for (int d = (tid & 1) * (D / 2); d < (tid & 1) * (D / 2) + D / 2; d += 4)
+                *(float4 *)(op + d) = float4{0.f, 0.f, 0.f, 0.f};
+            if ((tid & 1) == 0)
+                a.LSE[(size_t)cur.split * a.l_split + cur.row0 + r] = -INFINITY;
+        }
     }
 };
 
-template <int D, bool CAUSAL, bool OBF16>
+// A workgroup computes its items one after another as one stream of key
+// tiles: the DMA of the next item's first tile and the load of its Q overlap
+// the current item's last tile, and the current item's O stores overlap the
+// next item's first tile.  The grid is either one workgroup per item or two
+// resident workgroups per CU looping over the items (persistent).
+template <int D, bool CAUSAL, bool OBF16, bool PERSIST>
 __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(Args args)
 {
     using C = Cfg<D>;
-    // four distinct LDS objects, so the compiler can tell a DMA into one
-    // buffer from reads of another and need not wait for it
-    __shared__ __attribute__((aligned(16))) unsigned char kb0[C::TILE_BYTES];
-    __shared__ __attribute__((aligned(16))) unsigned char kb1[C::TILE_BYTES];
-    __shared__ __attribute__((aligned(16))) unsigned char vb0[C::TILE_BYTES];
-    __shared__ __attribute__((aligned(16))) unsigned char vb1[C::TILE_BYTES];
+    // two stages, each a K tile then a V tile
+    __shared__ __attribute__((aligned(16))) unsigned char lds[4 * C::TILE_BYTES];
 
-    Kernel<D, CAUSAL> k(args);
+    Kernel<D, CAUSAL, OBF16, PERSIST> k(args);
     const Args &a = args;
     const int tid = threadIdx.x;
     k.wave = tid >> 6;
     k.lane = tid & 63;
     k.col = k.lane & 31;
     k.half = k.lane >> 5;
+    k.off = a.Sk - a.Sq;
 
-    int head, qt, split;
-    decode_wg(a, blockIdx.x, head, qt, split);
-    if (CAUSAL)
-        qt = a.n_qt - 1 - qt;   // heaviest query tiles of a head first
-    const int b = head / a.Hq, hq = head % a.Hq;
-    const int hk = hq / a.group;
-    k.off = a.Sk - a.Sq;        // bottom-right causal offset
-    const int q0 = qt * BM;
-    k.qi = q0 + k.wave * 32 + k.col;
-    const int q_last_wg = min(q0 + BM, a.Sq) - 1;
-    k.q_last_wave = min(q0 + k.wave * 32 + 31, a.Sq - 1);
-    const bool wave_has_rows = q0 + k.wave * 32 < a.Sq;
-
-    // key tiles to visit, and the first one needing per-element masks
-    const int n_kv_all = (a.Sk + BN - 1) / BN;
-    int n_kv = n_kv_all;
-    int first_masked = (a.Sk % BN) ? n_kv_all - 1 : n_kv_all;
-    if (CAUSAL) {
-        n_kv = min(n_kv_all, (q_last_wg + k.off) / BN + 1);
-        first_masked = min(first_masked, max(0, (q0 + k.off + 1) / BN));
-        first_masked = min(first_masked, n_kv);
-    }
-
-    // this workgroup's key tiles: [j_lo, j_hi) of the visible ones
-    const int j_lo = split * a.split_tiles;
-    const int j_hi = min(n_kv, j_lo + a.split_tiles);
-    const size_t row0 = ((size_t)b * a.Hq + hq) * a.Sq;
-    if (j_lo >= j_hi) {
-        // no visible key of this split: an empty partial result
-        // (LSE = -inf, O = 0), which the combine step weights by zero
-        const int r = q0 + (int)tid / 2;
-        if (tid < 2 * BM && r < a.Sq) {
-            float *op = (float *)a.O + (size_t)split * a.o_split + (row0 + r) * D;
-#pragma unroll
-            for (int d = (tid & 1) * (D / 2); d < (tid & 1) * (D / 2) + D / 2; d += 4)
-                *(float4 *)(op + d) = float4{0.f, 0.f, 0.f, 0.f};
-            if ((tid & 1) == 0)
-                a.LSE[(size_t)split * a.l_split + row0 + r] = -INFINITY;
-        }
+    int L = static_item(a, blockIdx.x, gridDim.x, 0);
+    if (L < 0)
+        return;
+    k.cur = k.describe(L);
+    if (k.cur.j_lo >= k.cur.j_hi) {
+        // (key splits only: such a grid has one workgroup per item)
+        k.empty_result(tid);
         return;
     }
-
-    const size_t kv_base = ((size_t)b * a.Hkv + hk) * (size_t)a.Sk * D;
-    k.Kg = a.K + kv_base;
-    k.Vg = a.V + kv_base;
     k.init_dma();
-
-    // Q for this lane's query, as the B operand of S^T = K Q^T
-    {
-        const uint16_t *qp = a.Q + (((size_t)b * a.Hq + hq) * a.Sq + min(k.qi, a.Sq - 1)) * D +
-                             8 * k.half;
-#pragma unroll
-        for (int kk = 0; kk < C::KK; ++kk) {
-            u32x4 v = *(const u32x4 *)(qp + 16 * kk);
-            if (k.qi >= a.Sq)
-                v = u32x4{0u, 0u, 0u, 0u};
-            k.qreg[kk] = __builtin_bit_cast(bf16x8, v);
-        }
-    }
-#pragma unroll
-    for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-            k.acc_o[db][r] = 0.f;
-    k.m_run = -INFINITY;
-    k.l_run = 0.f;
-    k.m_trig = -INFINITY;
-
-    // wave w sees tile j unless every key in it is beyond its last query
-    auto active = [&](int j) {
-        return wave_has_rows && (!CAUSAL || j * BN <= k.q_last_wave + k.off);
-    };
-
-    // prologue: tile j_lo in flight
-    k.template dma_tile<false>(j_lo, kb0);
-    k.template dma_tile<true>(j_lo, vb0);
-    wait_dma();
+    k.set_rows();
+    k.load_q(k.cur);
+    // prologue: the first tile in stage 0
+    k.dma_kv(k.cur.kv_base, k.cur.j_lo, lds);
+    tileattn_dma::wait_vmcnt<0>();
     __syncthreads();
 
-    // Steady state, unrolled by two so every buffer reference is static.
-    // Every thread runs every iteration (all take part in the DMA and the
-    // barrier).  Tiles before first_masked are fully visible to every real
-    // query of the workgroup; a wave holding only padding rows (past Sq)
-    // computes on zero queries there and never stores.
-    // (buffer parity counts from j_lo)
-    const int j_fast = min(first_masked, j_hi);
-    int j = j_lo;
-    for (; j + 1 < j_fast; j += 2) {
-        k.fast_step(j, j_hi, kb0, kb1, vb0, vb1);
-        k.fast_step(j + 1, j_hi, kb1, kb0, vb1, vb0);
+    int st = 0;
+    for (int r = 1;; ++r) {
+        L = PERSIST ? static_item(a, blockIdx.x, gridDim.x, r) : -1;
+        k.has_next = L >= 0;
+        if (k.has_next)
+            k.nxt = k.describe(L);
+        k.reset_state();
+        st = k.run_item(lds, st);
+        if (!k.has_next)
+            break;
+        k.cur = k.nxt;
+        k.set_rows();
     }
-    if (j < j_fast) {
-        k.fast_step(j, j_hi, kb0, kb1, vb0, vb1);
-        ++j;
-    }
-
-    // Remaining tiles (masked): waves skip tiles they cannot see.
-    for (; j < j_hi; ++j) {
-        const bool odd = (j - j_lo) & 1;
-        const unsigned char *kc = odd ? kb1 : kb0;
-        unsigned char *kn = odd ? kb0 : kb1;
-        const unsigned char *vc = odd ? vb1 : vb0;
-        unsigned char *vn = odd ? vb0 : vb1;
-        if (j + 1 < j_hi) {
-            k.template dma_tile<false>(j + 1, kn);
-            k.template dma_tile<true>(j + 1, vn);
-        }
-        if (active(j)) {
-            f32x16 s[2];
-            k.scores(kc, s);
-            k.template row_max<true>(j, s);
-            k.template exp_pv<true>(s, vc);
-        }
-        wait_dma();
-        __syncthreads();
-    }
-
-    // epilogue: normalise, store O rows (fp32, or bf16 rounded to nearest
-    // even) and LSE.  A row that saw no key of its split (only possible with
-    // key splits) stores the empty partial result: O = 0, LSE = -inf.
-    //   The rows go through LDS so that every store instruction writes whole
-    // rows (lane (col, half) holds 4 consecutive dims of row col per (db, g):
-    // written directly, each instruction would be 32 pieces of 16 or 8
-    // bytes).  Each wave stages its 32 rows in its own quarter of the tile
-    // buffers, which every wave has left behind at the last tile's barrier;
-    // 16-byte chunk q of staged row r sits at q ^ (r % RCH).  A wave reads
-    // back only what it wrote itself (its LDS accesses complete in order).
-    const float l = sum_halves(k.l_run);
-    const bool empty = !(l > 0.f);
-    const float inv = empty ? 0.f : 1.f / l;
-    constexpr int EB = OBF16 ? 2 : 4;     // bytes per output element
-    constexpr int RCH = D * EB / 16;      // 16-byte chunks per row
-    constexpr int RPI = 64 / RCH;         // rows per store instruction
-    unsigned char *const stg = k.wave == 0 ? kb0 : k.wave == 1 ? kb1 : k.wave == 2 ? vb0 : vb1;
-#pragma unroll
-    for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const int byte = (32 * db + 8 * g + 4 * k.half) * EB;   // within the row
-            unsigned char *p =
-                stg + k.col * (D * EB) + (((byte >> 4) ^ (k.col & (RCH - 1))) * 16) + (byte & 15);
-            const float x0 = k.acc_o[db][4 * g + 0] * inv, x1 = k.acc_o[db][4 * g + 1] * inv;
-            const float x2 = k.acc_o[db][4 * g + 2] * inv, x3 = k.acc_o[db][4 * g + 3] * inv;
-            if (OBF16)
-                *(u32x2 *)p = u32x2{pack_bf16(x0, x1), pack_bf16(x2, x3)};
-            else
-                *(float4 *)p = float4{x0, x1, x2, x3};
-        }
-#pragma unroll
-    for (int it = 0; it < 32 / RPI; ++it) {
-        const int r = it * RPI + k.lane / RCH, q = k.lane % RCH;
-        const u32x4 v = *(const u32x4 *)(stg + r * (D * EB) + ((q ^ (r & (RCH - 1))) * 16));
-        const int qr = q0 + k.wave * 32 + r;
-        if (qr < a.Sq) {
-            if (OBF16)
-                *(u32x4 *)((uint16_t *)a.O + (row0 + qr) * D + 8 * q) = v;
-            else
-                *(u32x4 *)((float *)a.O + (size_t)split * a.o_split + (row0 + qr) * D + 4 * q) = v;
-        }
-    }
-    if (k.qi < a.Sq && k.half == 0)
-        a.LSE[(size_t)split * a.l_split + row0 + k.qi] =
-            empty ? -INFINITY : (k.m_run + log2f(l)) * LN2;
 }
 
+// One workgroup per item when `grid` covers the items, else the persistent
+// kernel (no key splits then).
 template <int D, bool CAUSAL, bool OBF16>
-hipError_t launch(const Args &a, hipStream_t stream)
+hipError_t launch(const Args &a, int grid, hipStream_t stream)
 {
-    hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, OBF16>), dim3(a.n_wg), dim3(NT), 0, stream, a);
+    if (grid < a.n_items)
+        hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, OBF16, true>), dim3(grid), dim3(NT), 0,
+                           stream, a);
+    else
+        hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, OBF16, false>), dim3(grid), dim3(NT), 0,
+                           stream, a);
     return hipGetLastError();
+}
+
+// Workgroups of the attention kernel resident at once per CU (its LDS, four
+// tile buffers, and registers allow two).  A causal grid with more items
+// than resident workgroups is launched persistent: this many workgroups per
+// CU, each looping over its share of the items (measured on one MI355X:
+// grouped-query S=4096 +6 %, B=1 H=32 S=4096 +10 %, S=8192 unchanged).
+// Non-causal items all cost the same, and there the grid of one workgroup
+// per item measured 4-5 % faster than the persistent one (B=8 H=32 S=2048).
+#ifndef TA_RESIDENT_PER_CU
+#define TA_RESIDENT_PER_CU 2
+#endif
+constexpr int MAX_DEVICES = 64;
+std::atomic<int> cu_count[MAX_DEVICES];
+
+// Grid size for n_items work items on the current device (one workgroup per
+// item unless the persistent grid is smaller; a multiple of the XCD count).
+int grid_size(int n_items, int n_split, bool causal)
+{
+    if (TA_RESIDENT_PER_CU < 1 || n_split != 1 || !causal)
+        return n_items;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES)
+        return n_items;
+    int n = cu_count[dev].load(std::memory_order_relaxed);
+    if (n <= 0) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            n <= 0)
+            return n_items;
+        cu_count[dev].store(n, std::memory_order_relaxed);
+    }
+    const int g = (TA_RESIDENT_PER_CU * n) / NXCD * NXCD;
+    return g >= NXCD && n_items > g ? g : n_items;
 }
 
 bool overlaps(const void *p, size_t pn, const void *q, size_t qn)
@@ -625,10 +799,10 @@ ta_status attn_fwd_any(const void *Q, const void *K, const void *V, void *O, boo
     // 32-bit in-kernel offsets are used within one (batch, head) slice only;
     // the grid itself must fit a 32-bit workgroup count
     const int64_t n_qt = ((int64_t)Sq + BM - 1) / BM;
-    const int64_t n_wg = (int64_t)B * Hq * n_qt * n_split;
+    const int64_t n_items = (int64_t)B * Hq * n_qt * n_split;
     const int64_t n_rows = (int64_t)B * Hq * Sq;
     if ((int64_t)Sq * D >= (1ll << 31) || (int64_t)Sk * D >= (1ll << 31) ||
-        n_wg >= (1ll << 31) || n_rows >= (1ll << 31))
+        n_items >= (1ll << 31) || n_rows >= (1ll << 31))
         return TA_ERR_INVALID_SHAPE;
     if (misaligned(Q) || misaligned(K) || misaligned(V) || misaligned(O) || misaligned(LSE))
         return TA_ERR_MISALIGNED;
@@ -669,7 +843,7 @@ ta_status attn_fwd_any(const void *Q, const void *K, const void *V, void *O, boo
     a.n_qt = (int)n_qt;
     a.n_split = n_split;
     a.split_tiles = split_tiles;
-    a.n_wg = (int)n_wg;
+    a.n_items = (int)n_items;
     a.c = scale * LOG2E;
     // split partial results: O then LSE of every split (no workspace for one split)
     float *Op = (float *)ws;
@@ -687,18 +861,19 @@ ta_status attn_fwd_any(const void *Q, const void *K, const void *V, void *O, boo
     }
 
     hipStream_t s = (hipStream_t)stream;
+    const int grid = grid_size(a.n_items, n_split, causal != 0);
     hipError_t e;
     const bool kb = o_bf16 && n_split == 1;   // the attention kernel writes bf16 O itself
     if (kb) {
         if (D == 64)
-            e = causal ? launch<64, true, true>(a, s) : launch<64, false, true>(a, s);
+            e = causal ? launch<64, true, true>(a, grid, s) : launch<64, false, true>(a, grid, s);
         else
-            e = causal ? launch<128, true, true>(a, s) : launch<128, false, true>(a, s);
+            e = causal ? launch<128, true, true>(a, grid, s) : launch<128, false, true>(a, grid, s);
     } else {
         if (D == 64)
-            e = causal ? launch<64, true, false>(a, s) : launch<64, false, false>(a, s);
+            e = causal ? launch<64, true, false>(a, grid, s) : launch<64, false, false>(a, grid, s);
         else
-            e = causal ? launch<128, true, false>(a, s) : launch<128, false, false>(a, s);
+            e = causal ? launch<128, true, false>(a, grid, s) : launch<128, false, false>(a, grid, s);
     }
     if (e == hipSuccess && n_split > 1) {
         const int nr = (int)n_rows;
@@ -714,7 +889,6 @@ ta_status attn_fwd_any(const void *Q, const void *K, const void *V, void *O, boo
 
 // Per-device address of `tileattn_split_scratch` (declared below, outside
 // this namespace), looked up once per device with that device current.
-constexpr int MAX_DEVICES = 64;
 std::atomic<void *> scratch_addr[MAX_DEVICES];
 
 }  // namespace

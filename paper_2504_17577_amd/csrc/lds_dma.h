@@ -44,6 +44,18 @@ __device__ __forceinline__ void dma16(uint32_t lds, uint32_t voff, u32x4s rsrc)
                  : "memory");
 }
 
+// The same with a wave-uniform byte offset `soff` (a scalar register) added to
+// the lane's `voff`.
+__device__ __forceinline__ void dma16_soff(uint32_t lds, uint32_t voff, uint32_t soff,
+                                           u32x4s rsrc)
+{
+    asm volatile("s_nop 0\n\t"
+                 "buffer_load_dwordx4 %0, %1, %2 offen lds"
+                 :
+                 : "v"(voff), "s"(rsrc), "s"(soff), "{m0}"(__builtin_amdgcn_readfirstlane(lds))
+                 : "memory");
+}
+
 __device__ __forceinline__ uint32_t lds_addr(const void *p)
 {
     return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
