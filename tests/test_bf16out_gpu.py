@@ -34,6 +34,8 @@ CASES = [
     ("ragged_d64", 2, 6, 3, 65, 63, 64, False),
     ("dense_d128_s2k",) + (8, 32, 32, 2048, 2048, 128, False),
     ("chunk_causal_d128_q1k_k8k",) + (1, 32, 8, 1024, 8192, 128, True),
+    ("persistent_ragged_gqa_causal", 4, 20, 5, 1000, 1037, 64, True),
+    ("persistent_gqa_causal_d128", 5, 24, 3, 777, 900, 128, True),
 ]
 
 

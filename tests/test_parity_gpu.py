@@ -193,6 +193,25 @@ def test_edge_shapes(ta, shape):
     compare_full(ta, q, k, v, causal, 1.0 / math.sqrt(D), str(shape))
 
 
+# Causal launches with more query tiles than two per CU (512 on 256 CUs) run
+# on the persistent grid: ragged Sq and Sk, grouped-query heads, both head
+# dims, more items than a multiple of the workgroups.
+PERSISTENT = [
+    # (B, Hq, Hkv, Sq, Sk, D, causal)
+    (4, 20, 5, 1000, 1037, 64, True),
+    (5, 24, 3, 777, 900, 128, True),
+    (2, 40, 40, 897, 897, 128, True),
+]
+
+
+@pytest.mark.parametrize("shape", PERSISTENT, ids=[str(s) for s in PERSISTENT])
+def test_persistent_grid_shapes(ta, shape):
+    B, Hq, Hkv, Sq, Sk, D, causal = shape
+    assert B * Hq * -(-Sq // 128) > 512   # more query tiles than resident workgroups
+    q, k, v = gen.random_problem(B, Hq, Hkv, Sq, Sk, D, seed=sum(shape))
+    compare_full(ta, q, k, v, causal, 1.0 / math.sqrt(D), str(shape))
+
+
 def test_causal_row0_is_v0(ta):
     """Query 0 sees key 0 only.  Its weight is exp2 of the rounding residual of
     the max score (about 1 +- 2^-22) and rounds to exactly 1.0 in bf16, while
