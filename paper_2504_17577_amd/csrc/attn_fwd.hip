@@ -69,6 +69,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -78,6 +79,7 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(1))) void glb_void;
 
 constexpr int BM = 128;      // query rows per workgroup (4 waves x 32)
+constexpr int BM_SMALL = 64; // the same with 16 query rows per wave (small grids)
 constexpr int BN = 64;       // keys per tile
 constexpr int NT = 256;      // threads per workgroup
 constexpr int NXCD = 8;      // XCDs per MI355X
@@ -122,9 +124,14 @@ struct Args {
     float c;         // scale * log2(e)
 };
 
-__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c)
+__device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c)
 {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
@@ -144,6 +151,21 @@ __device__ __forceinline__ float max_halves(float x)
 __device__ __forceinline__ float sum_halves(float x)
 {
     const u32x2 r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                     false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// the same over lanes l and l ^ 16
+__device__ __forceinline__ float max_rows16(float x)
+{
+    const u32x2 r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x),
+                                                     false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float sum_rows16(float x)
+{
+    const u32x2 r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x),
                                                      false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
@@ -189,12 +211,25 @@ struct Item {
     size_t kv_base;  // (b * Hkv + hk) * Sk * D: the head's K/V slice
 };
 
-template <int D, bool CAUSAL, bool OBF16, bool PERSIST>
+// QW = 32 or 16 query rows per wave.  QW = 32: S^T and O^T blocks of
+// v_mfma_f32_32x32x16_bf16, lane l owns query l % 32 and half l / 32 of
+// each block's rows.  QW = 16: blocks of v_mfma_f32_16x16x32_bf16, lane l
+// owns query l % 16 and quarter l / 16 (64-query workgroups, for grids
+// that leave the CUs short of waves).
+template <int D, int QW, bool CAUSAL, bool OBF16, bool PERSIST>
 struct Kernel {
     using C = Cfg<D>;
+    static constexpr int BMQ = 4 * QW;                     // query rows per workgroup
+    static constexpr int NKB = BN / QW;                    // key blocks of a tile
+    static constexpr int KK = QW == 32 ? D / 16 : D / 32;  // k-steps of the scores
+    static constexpr int DB = D / QW;                      // row blocks of O^T
+    static constexpr int NG = 64 / QW;                     // lanes per query
+    using Acc = typename std::conditional<QW == 32, f32x16, f32x4>::type;
+    static constexpr int AR = QW == 32 ? 16 : 4;           // accumulator values per block
 
     const Args &a;
-    int wave, lane, col, half;
+    int wave, lane;
+    int col, half;           // lane % QW (the query), lane / QW
     int wave_u;              // the wave index, in a scalar register
     int off;                 // Sk - Sq, the bottom-right causal offset
     Item cur, nxt;           // the item being computed and the workgroup's next one
@@ -202,8 +237,8 @@ struct Kernel {
     int qi, q_last_wave;     // this lane's query row; last real row of the wave
     bool wave_has_rows;
     uint32_t koff, voff;     // byte offsets of this lane's first K / V chunk in a tile
-    bf16x8 qreg[C::KK];
-    f32x16 acc_o[C::DB];
+    bf16x8 qreg[KK];
+    Acc acc_o[DB];
     float m_run, l_run;
     float m_trig;   // the running max is raised when a tile max exceeds this
 
@@ -220,7 +255,7 @@ struct Kernel {
             qt = a.n_qt - 1 - qt;   // heaviest query tiles of a head first
         const int b = head / a.Hq, hq = head % a.Hq;
         const int hk = hq / a.group;
-        it.q0 = qt * BM;
+        it.q0 = qt * BMQ;
         it.row0 = ((size_t)b * a.Hq + hq) * a.Sq;
         it.kv_base = ((size_t)b * a.Hkv + hk) * (size_t)a.Sk * D;
         // key tiles to visit, and the first one needing per-element masks
@@ -228,7 +263,7 @@ struct Kernel {
         int n_kv = n_kv_all;
         int first_masked = (a.Sk % BN) ? n_kv_all - 1 : n_kv_all;
         if (CAUSAL) {
-            const int q_last_wg = min(it.q0 + BM, a.Sq) - 1;
+            const int q_last_wg = min(it.q0 + BMQ, a.Sq) - 1;
             n_kv = min(n_kv_all, (q_last_wg + off) / BN + 1);
             first_masked = min(first_masked, max(0, (it.q0 + off + 1) / BN));
             first_masked = min(first_masked, n_kv);
@@ -243,17 +278,17 @@ struct Kernel {
     // index in a scalar register, so that branches on them are uniform)
     __device__ __forceinline__ void set_rows()
     {
-        qi = cur.q0 + wave * 32 + col;
-        q_last_wave = min(cur.q0 + wave_u * 32 + 31, a.Sq - 1);
-        wave_has_rows = cur.q0 + wave_u * 32 < a.Sq;
+        qi = cur.q0 + wave * QW + col;
+        q_last_wave = min(cur.q0 + wave_u * QW + QW - 1, a.Sq - 1);
+        wave_has_rows = cur.q0 + wave_u * QW < a.Sq;
     }
 
     __device__ __forceinline__ void reset_state()
     {
 #pragma unroll
-        for (int db = 0; db < C::DB; ++db)
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
+            for (int r = 0; r < AR; ++r)
                 acc_o[db][r] = 0.f;
         m_run = -INFINITY;
         l_run = 0.f;
@@ -265,11 +300,12 @@ struct Kernel {
     // results are never stored.
     __device__ __forceinline__ void load_q(const Item &it)
     {
-        const int r = min(it.q0 + wave * 32 + col, a.Sq - 1);
+        // (dims 8 NG kk + 8 half .. +7 for k-step kk)
+        const int r = min(it.q0 + wave * QW + col, a.Sq - 1);
         const uint16_t *qp = a.Q + (it.row0 + r) * D + 8 * half;
 #pragma unroll
-        for (int kk = 0; kk < C::KK; ++kk)
-            qreg[kk] = __builtin_bit_cast(bf16x8, *(const u32x4 *)(qp + 16 * kk));
+        for (int kk = 0; kk < KK; ++kk)
+            qreg[kk] = __builtin_bit_cast(bf16x8, *(const u32x4 *)(qp + 8 * NG * kk));
     }
 
     // Each lane's source byte offset (within a tile) for its 16-byte LDS
@@ -327,45 +363,53 @@ struct Kernel {
         dma_tile<true>(a.V + kv_base, j, stage + C::TILE_BYTES);
     }
 
-    // S^T[key][query] of one tile (two 32-key blocks, chains interleaved)
-    __device__ __forceinline__ void scores(const unsigned char *kbuf, f32x16 (&s)[2]) const
+    // S^T[key][query] of one tile (NKB blocks of QW keys, chains interleaved)
+    __device__ __forceinline__ void scores(const unsigned char *kbuf, Acc (&s)[NKB]) const
     {
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < NKB; ++b)
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
+            for (int r = 0; r < AR; ++r)
                 s[b][r] = 0.f;
 #pragma unroll
-        for (int kk = 0; kk < C::KK; ++kk)
+        for (int kk = 0; kk < KK; ++kk)
 #pragma unroll
-            for (int b = 0; b < 2; ++b) {
-                const int row = 32 * b + col;
-                const int ch = (2 * kk + half) ^ C::kswz(row);
+            for (int b = 0; b < NKB; ++b) {
+                const int row = QW * b + col;
+                const int ch = (NG * kk + half) ^ C::kswz(row);
                 const bf16x8 av = *(const bf16x8 *)(kbuf + row * (D * 2) + ch * 16);
-                s[b] = mfma32(av, qreg[kk], s[b]);
+                s[b] = mfma(av, qreg[kk], s[b]);
             }
+    }
+
+    // key (within the tile) of accumulator value r of block b
+    __device__ __forceinline__ int key_of(int b, int r) const
+    {
+        return QW == 32 ? 32 * b + 8 * (r >> 2) + 4 * half + (r & 3) : 16 * b + 4 * half + r;
     }
 
     // Online softmax, first half: mask, row max, and (when some row's tile
     // max passes its level m_trig) raise the running max and rescale the
     // accumulator.
     template <bool MASKED>
-    __device__ __forceinline__ void row_max(int j, f32x16 (&s)[2])
+    __device__ __forceinline__ void row_max(int j, Acc (&s)[NKB])
     {
-        // lane holds keys j*BN + 32b + 8(r/4) + 4half + r%4 of query qi
+        // lane holds keys j*BN + key_of(b, r) of query qi
         float mx = -INFINITY;
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < NKB; ++b)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
+            for (int r = 0; r < AR; ++r) {
                 if (MASKED) {
-                    const int key = j * BN + 32 * b + 8 * (r >> 2) + 4 * half + (r & 3);
+                    const int key = j * BN + key_of(b, r);
                     const bool ok = key < a.Sk && (!CAUSAL || key <= qi + off);
                     s[b][r] = ok ? s[b][r] : -INFINITY;
                 }
                 mx = fmaxf(mx, s[b][r]);
             }
         mx = max_halves(mx);
+        if (QW == 16)
+            mx = max_rows16(mx);
         const float m_tile = MASKED && mx == -INFINITY ? -INFINITY : mx * a.c;
         // raise the running max when some row passes its level (a
         // wave-uniform decision; every lane of the wave then rescales, by 1
@@ -380,9 +424,9 @@ struct Kernel {
             m_run = m_new;
             l_run *= alpha;
 #pragma unroll
-            for (int db = 0; db < C::DB; ++db)
+            for (int db = 0; db < DB; ++db)
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
+                for (int r = 0; r < AR; ++r)
                     acc_o[db][r] *= alpha;
         }
     }
@@ -390,15 +434,15 @@ struct Kernel {
     // Online softmax, second half: weights exp2(c*s - m), row sum, bf16
     // weights, then O^T += V^T P^T
     template <bool MASKED>
-    __device__ __forceinline__ void exp_pv(const f32x16 (&s)[2], const unsigned char *vbuf)
+    __device__ __forceinline__ void exp_pv(const Acc (&s)[NKB], const unsigned char *vbuf)
     {
         const float m_use = MASKED && m_run == -INFINITY ? 0.f : m_run;
         float rowsum = 0.f;
-        uint32_t pk[2][8];
+        uint32_t pk[NKB][AR / 2];
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < NKB; ++b)
 #pragma unroll
-            for (int r = 0; r < 16; r += 2) {
+            for (int r = 0; r < AR; r += 2) {
                 float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][r], a.c, -m_use));
                 float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][r + 1], a.c, -m_use));
                 if (MASKED) {
@@ -414,31 +458,61 @@ struct Kernel {
         m_trig = m_run + fminf(RESCALE_SLACK,
                                fmaxf(0.f, RAISE_SHARE_LOG2 + __builtin_amdgcn_logf(l_run)));
 
-        // MFMA k-slot t of half h stands for key 16ks + 4h + t (t < 4) or
-        // 16ks + 8 + 4h + t-4, matching where the accumulator layout left P
-        const int gq = lane >> 4, sl = lane & 15;
+        // The A operand (V^T) comes from the row-major V tile through the
+        // transpose read ds_read_b64_tr_b16: in each group of 16 lanes, lane
+        // 4i + c reads dims d0 + 4c .. d0 + 4c + 3 of key row r0 + i, and lane
+        // j of the group receives dim d0 + j of rows r0 .. r0 + 3, one dim
+        // over 4 consecutive keys.
+        const int sl = lane & 15;
+        if constexpr (QW == 32) {
+            // MFMA k-slot t of half h stands for key 16ks + 4h + t (t < 4) or
+            // 16ks + 8 + 4h + t-4, matching where the accumulator layout left P
+            const int gq = lane >> 4;
 #pragma unroll
-        for (int ks = 0; ks < BN / 16; ++ks) {
-            const int b = ks >> 1, rb = (ks & 1) * 4;
-            const u32x4 bw = {pk[b][rb], pk[b][rb + 1], pk[b][rb + 2], pk[b][rb + 3]};
-            const bf16x8 bv = __builtin_bit_cast(bf16x8, bw);
-            const int row0 = 16 * ks + 4 * half + (sl >> 2);
-            const int row1 = row0 + 8;
+            for (int ks = 0; ks < BN / 16; ++ks) {
+                const int b = ks >> 1, rb = (ks & 1) * 4;
+                const u32x4 bw = {pk[b][rb], pk[b][rb + 1], pk[b][rb + 2], pk[b][rb + 3]};
+                const bf16x8 bv = __builtin_bit_cast(bf16x8, bw);
+                const int row0 = 16 * ks + 4 * half + (sl >> 2);
+                const int row1 = row0 + 8;
 #pragma unroll
-            for (int db = 0; db < C::DB; ++db) {
-                const int d = 32 * db + 16 * (gq & 1) + 4 * (sl & 3);
-                const int byte_in = (2 * d) & 15;
-                const unsigned char *p0 =
-                    vbuf + row0 * (D * 2) + ((d >> 3) ^ C::vswz(row0)) * 16 + byte_in;
-                const unsigned char *p1 =
-                    vbuf + row1 * (D * 2) + ((d >> 3) ^ C::vswz(row1)) * 16 + byte_in;
-                const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p0);
-                const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p1);
-                const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
-                const u32x4 aw = {l2[0], l2[1], h2[0], h2[1]};
-                acc_o[db] = mfma32(__builtin_bit_cast(bf16x8, aw), bv, acc_o[db]);
+                for (int db = 0; db < DB; ++db) {
+                    const int d = 32 * db + 16 * (gq & 1) + 4 * (sl & 3);
+                    acc_o[db] = mfma(v_operand(vbuf, row0, row1, d), bv, acc_o[db]);
+                }
+            }
+        } else {
+            // MFMA k-slot t of quarter g stands for key 32ks + 4g + t (t < 4)
+            // or 32ks + 16 + 4g + t-4: blocks 2ks and 2ks+1 of the scores
+#pragma unroll
+            for (int ks = 0; ks < BN / 32; ++ks) {
+                const u32x4 bw = {pk[2 * ks][0], pk[2 * ks][1], pk[2 * ks + 1][0],
+                                  pk[2 * ks + 1][1]};
+                const bf16x8 bv = __builtin_bit_cast(bf16x8, bw);
+                const int row0 = 32 * ks + 4 * half + (sl >> 2);
+                const int row1 = row0 + 16;
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    const int d = 16 * db + 4 * (sl & 3);
+                    acc_o[db] = mfma(v_operand(vbuf, row0, row1, d), bv, acc_o[db]);
+                }
             }
         }
+    }
+
+    // 4 dims from d of V rows row0 (k-slots 0..3) and row1 (k-slots 4..7),
+    // transposed across lanes (see above)
+    __device__ __forceinline__ bf16x8 v_operand(const unsigned char *vbuf, int row0, int row1,
+                                                int d) const
+    {
+        const int byte_in = (2 * d) & 15;
+        const unsigned char *p0 = vbuf + row0 * (D * 2) + ((d >> 3) ^ C::vswz(row0)) * 16 + byte_in;
+        const unsigned char *p1 = vbuf + row1 * (D * 2) + ((d >> 3) ^ C::vswz(row1)) * 16 + byte_in;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p0);
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p1);
+        const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+        const u32x4 aw = {l2[0], l2[1], h2[0], h2[1]};
+        return __builtin_bit_cast(bf16x8, aw);
     }
 
     // wave w sees tile j unless every key in it is beyond its last query
@@ -462,7 +536,7 @@ struct Kernel {
         if (!last || has_next)
             dma_kv(last ? nxt.kv_base : cur.kv_base, last ? nxt.j_lo : j + 1, sn);
         const bool act = !MASKED || active(j);   // wave-uniform
-        f32x16 s[2];
+        Acc s[NKB];
         if (act)
             scores(sc, s);
         if (last && has_next) {
@@ -484,13 +558,13 @@ struct Kernel {
     // (only possible with key splits) stores the empty partial result:
     // O = 0, LSE = -inf.
     //   The rows go through LDS so that every store instruction writes whole
-    // rows (lane (col, half) holds 4 consecutive dims of row col per (db, g):
-    // written directly, each instruction would be 32 pieces of 16 or 8
+    // rows (lane (col, half) holds runs of 4 consecutive dims of row col:
+    // written directly, each instruction would write pieces of 16 or 8
     // bytes).  The staging area is the stage of the item's last tile, which
     // every wave has left behind at that tile's barrier (the other stage
     // holds the next item's first tile, in flight), or all of LDS in a grid
     // of one workgroup per item; each wave
-    // stages RP of its 32 rows at a time in its own quarter, 16-byte chunk q
+    // stages RP of its QW rows at a time in its own quarter, 16-byte chunk q
     // of staged row r at q ^ (r % RCH), and reads back only what it wrote
     // itself (a wave's LDS accesses complete in order).  A barrier then
     // keeps the next item's DMA into this stage behind every wave's reads;
@@ -499,7 +573,7 @@ struct Kernel {
     template <bool WHOLE_LDS>
     __device__ __forceinline__ void epilogue(unsigned char *stage)
     {
-        const float l = sum_halves(l_run);
+        const float l = QW == 32 ? sum_halves(l_run) : sum_rows16(sum_halves(l_run));
         const bool empty = !(l > 0.f);
         const float inv = empty ? 0.f : 1.f / l;
         constexpr int EB = OBF16 ? 2 : 4;               // bytes per output element
@@ -508,10 +582,10 @@ struct Kernel {
         // each wave's quarter of the staging area: of the last tile's stage,
         // or (WHOLE_LDS: one item per workgroup, no DMA in flight) of all of LDS
         constexpr int QB = (WHOLE_LDS ? 4 : 2) * C::TILE_BYTES / 4;
-        constexpr int RP = QB / (D * EB) < 32 ? QB / (D * EB) : 32;  // rows per pass
-        constexpr int NP = 32 / RP;                     // passes
+        constexpr int RP = QB / (D * EB) < QW ? QB / (D * EB) : QW;  // rows per pass
+        constexpr int NP = QW / RP;                     // passes
         constexpr int NI = RP / RPI;                    // reads per pass
-        static_assert(RP % RPI == 0 && 32 % RP == 0, "staging shape");
+        static_assert(RP % RPI == 0 && QW % RP == 0, "staging shape");
         unsigned char *const stg = stage + wave * QB;
         // O elements of this item's first row (the split's partial results
         // start o_split elements apart; bf16 O is never split)
@@ -525,11 +599,14 @@ struct Kernel {
         for (int p = 0; p < NP; ++p) {
             if (col / RP == p) {
                 const int r = col % RP;
+                // accumulator values 4g .. 4g+3 of block db: dims
+                // QW db + (QW == 32 ? 8 g + 4 half : 4 half) .. +3
 #pragma unroll
-                for (int db = 0; db < C::DB; ++db)
+                for (int db = 0; db < DB; ++db)
 #pragma unroll
-                    for (int g = 0; g < 4; ++g) {
-                        const int byte = (32 * db + 8 * g + 4 * half) * EB;   // within the row
+                    for (int g = 0; g < AR / 4; ++g) {
+                        const int dim = QW * db + (QW == 32 ? 8 * g : 0) + 4 * half;
+                        const int byte = dim * EB;   // within the row
                         unsigned char *pp =
                             stg + r * (D * EB) + (((byte >> 4) ^ (r & (RCH - 1))) * 16) + (byte & 15);
                         const float x0 = acc_o[db][4 * g + 0] * inv, x1 = acc_o[db][4 * g + 1] * inv;
@@ -552,7 +629,7 @@ struct Kernel {
             for (int it = 0; it < NI; ++it) {
                 const int r = it * RPI + lane / RCH, q = lane % RCH;
                 const u32x4 v = *(const u32x4 *)(stg + r * (D * EB) + ((q ^ (r & (RCH - 1))) * 16));
-                const int qr = cur.q0 + wave * 32 + p * RP + r;
+                const int qr = cur.q0 + wave * QW + p * RP + r;
                 if (qr < a.Sq) {
                     if (OBF16)
                         *(u32x4 *)((uint16_t *)a.O + obase + (size_t)qr * D + 8 * q) = v;
@@ -611,7 +688,7 @@ struct Kernel {
     __device__ void empty_result(int tid) const
     {
         const int r = cur.q0 + tid / 2;
-        if (tid < 2 * BM && r < a.Sq) {
+        if (tid < 2 * BMQ && r < a.Sq) {
             float *op = (float *)a.O + (size_t)cur.split * a.o_split + (cur.row0 + r) * D;
 #pragma unroll
             for (int d = (tid & 1) * (D / 2); d < (tid & 1) * (D / 2) + D / 2; d += 4)
@@ -626,21 +703,23 @@ struct Kernel {
 // tiles: the DMA of the next item's first tile and the load of its Q overlap
 // the current item's last tile, and the current item's O stores overlap the
 // next item's first tile.  The grid is either one workgroup per item or two
-// resident workgroups per CU looping over the items (persistent).
-template <int D, bool CAUSAL, bool OBF16, bool PERSIST>
-__global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(Args args)
+// resident workgroups per CU looping over the items (persistent).  QW = 16
+// workgroups use half the registers, so up to four fit a CU where LDS
+// allows (D = 64).
+template <int D, int QW, bool CAUSAL, bool OBF16, bool PERSIST>
+__global__ __launch_bounds__(NT, QW == 16 && D == 64 ? 4 : 2) void attn_fwd_kernel(Args args)
 {
     using C = Cfg<D>;
     // two stages, each a K tile then a V tile
     __shared__ __attribute__((aligned(16))) unsigned char lds[4 * C::TILE_BYTES];
 
-    Kernel<D, CAUSAL, OBF16, PERSIST> k(args);
+    Kernel<D, QW, CAUSAL, OBF16, PERSIST> k(args);
     const Args &a = args;
     const int tid = threadIdx.x;
     k.wave = tid >> 6;
     k.lane = tid & 63;
-    k.col = k.lane & 31;
-    k.half = k.lane >> 5;
+    k.col = k.lane % QW;
+    k.half = k.lane / QW;
     k.off = a.Sk - a.Sq;
 
     int L = static_item(a, blockIdx.x, gridDim.x, 0);
@@ -676,15 +755,19 @@ __global__ __launch_bounds__(NT, 2) void attn_fwd_kernel(Args args)
 }
 
 // One workgroup per item when `grid` covers the items, else the persistent
-// kernel (no key splits then).
+// kernel (no key splits then); 64-query workgroups (16 rows per wave) for
+// small grids, one workgroup per item.
 template <int D, bool CAUSAL, bool OBF16>
-hipError_t launch(const Args &a, int grid, hipStream_t stream)
+hipError_t launch(const Args &a, int grid, bool small, hipStream_t stream)
 {
-    if (grid < a.n_items)
-        hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, OBF16, true>), dim3(grid), dim3(NT), 0,
+    if (small)
+        hipLaunchKernelGGL((attn_fwd_kernel<D, 16, CAUSAL, OBF16, false>), dim3(grid), dim3(NT),
+                           0, stream, a);
+    else if (grid < a.n_items)
+        hipLaunchKernelGGL((attn_fwd_kernel<D, 32, CAUSAL, OBF16, true>), dim3(grid), dim3(NT), 0,
                            stream, a);
     else
-        hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, OBF16, false>), dim3(grid), dim3(NT), 0,
+        hipLaunchKernelGGL((attn_fwd_kernel<D, 32, CAUSAL, OBF16, false>), dim3(grid), dim3(NT), 0,
                            stream, a);
     return hipGetLastError();
 }
@@ -702,25 +785,45 @@ hipError_t launch(const Args &a, int grid, hipStream_t stream)
 constexpr int MAX_DEVICES = 64;
 std::atomic<int> cu_count[MAX_DEVICES];
 
-// Grid size for n_items work items on the current device (one workgroup per
-// item unless the persistent grid is smaller; a multiple of the XCD count).
-int grid_size(int n_items, int n_split, bool causal)
+// CUs of the current device (0 if the runtime cannot tell), looked up once
+// per device.
+int current_cu_count()
 {
-    if (TA_RESIDENT_PER_CU < 1 || n_split != 1 || !causal)
-        return n_items;
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES)
-        return n_items;
+        return 0;
     int n = cu_count[dev].load(std::memory_order_relaxed);
     if (n <= 0) {
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
             n <= 0)
-            return n_items;
+            return 0;
         cu_count[dev].store(n, std::memory_order_relaxed);
     }
-    const int g = (TA_RESIDENT_PER_CU * n) / NXCD * NXCD;
+    return n;
+}
+
+// Grid size for n_items work items on a device with n_cu CUs (one
+// workgroup per item unless the persistent grid is smaller; a multiple of
+// the XCD count).
+int grid_size(int n_items, int n_split, bool causal, int n_cu)
+{
+    if (TA_RESIDENT_PER_CU < 1 || n_split != 1 || !causal)
+        return n_items;
+    const int g = (TA_RESIDENT_PER_CU * n_cu) / NXCD * NXCD;
     return g >= NXCD && n_items > g ? g : n_items;
 }
+
+// Grids of 128-query tiles that would leave at least half of the CUs
+// without a workgroup run as 64-query workgroups (16 query rows per wave)
+// instead: twice the workgroups, each wave's chain of key tiles half as long
+// in MFMA and softmax work (measured on one MI355X: B=1 H=32 S=512 causal
+// 134 -> 170 and non-causal 288 -> 340 TFLOP/s).  Where the 64-query grid
+// would put two workgroups on a CU it measured 2-9 % slower than the
+// 128-query grid (its waves read each K/V tile from LDS for half as many
+// queries), so larger grids keep 128-query tiles.
+#ifndef TA_SMALL_TILES
+#define TA_SMALL_TILES 1
+#endif
 
 bool overlaps(const void *p, size_t pn, const void *q, size_t qn)
 {
@@ -861,19 +964,29 @@ ta_status attn_fwd_any(const void *Q, const void *K, const void *V, void *O, boo
     }
 
     hipStream_t s = (hipStream_t)stream;
-    const int grid = grid_size(a.n_items, n_split, causal != 0);
+    const int n_cu = current_cu_count();
+    const bool small = TA_SMALL_TILES && n_split == 1 && n_cu > 0 && 2 * n_items <= (int64_t)n_cu;
+    if (small) {
+        a.n_qt = (Sq + BM_SMALL - 1) / BM_SMALL;
+        a.n_items = B * Hq * a.n_qt;
+    }
+    const int grid = small ? a.n_items : grid_size(a.n_items, n_split, causal != 0, n_cu);
     hipError_t e;
     const bool kb = o_bf16 && n_split == 1;   // the attention kernel writes bf16 O itself
     if (kb) {
         if (D == 64)
-            e = causal ? launch<64, true, true>(a, grid, s) : launch<64, false, true>(a, grid, s);
+            e = causal ? launch<64, true, true>(a, grid, small, s)
+                       : launch<64, false, true>(a, grid, small, s);
         else
-            e = causal ? launch<128, true, true>(a, grid, s) : launch<128, false, true>(a, grid, s);
+            e = causal ? launch<128, true, true>(a, grid, small, s)
+                       : launch<128, false, true>(a, grid, small, s);
     } else {
         if (D == 64)
-            e = causal ? launch<64, true, false>(a, grid, s) : launch<64, false, false>(a, grid, s);
+            e = causal ? launch<64, true, false>(a, grid, small, s)
+                       : launch<64, false, false>(a, grid, small, s);
         else
-            e = causal ? launch<128, true, false>(a, grid, s) : launch<128, false, false>(a, grid, s);
+            e = causal ? launch<128, true, false>(a, grid, small, s)
+                       : launch<128, false, false>(a, grid, small, s);
     }
     if (e == hipSuccess && n_split > 1) {
         const int nr = (int)n_rows;

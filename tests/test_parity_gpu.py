@@ -183,6 +183,9 @@ EDGE = [
     (1, 4, 4, 1, 1000, 128, True), (1, 4, 4, 1000, 37, 128, False),
     (2, 6, 3, 65, 63, 64, False), (1, 16, 2, 300, 300, 128, True),
     (1, 2, 2, 128, 129, 64, True), (1, 2, 2, 256, 256, 128, False),
+    # more than 128 query tiles of 128 rows (launched with 128-query
+    # workgroups; the shapes above run as 64-query workgroups), ragged
+    (3, 16, 16, 700, 700, 64, True), (2, 40, 8, 1000, 1100, 128, False),
 ]
 
 
