@@ -121,6 +121,7 @@ struct Args {
     int n_split;     // key-range splits per query tile
     int split_tiles; // key tiles per split
     int n_items;     // work items: B * Hq * n_qt * n_split
+    int cu_per_xcd;  // CUs of one XCD (0: unknown)
     float c;         // scale * log2(e)
 };
 
@@ -185,20 +186,35 @@ __device__ __forceinline__ int xcd_range_n(const Args &a, int x)
     return a.n_items / NXCD + (x < a.n_items % NXCD ? 1 : 0);
 }
 
-// Workgroup bid's item of round r (-1 past the end of its XCD's range).
-// The workgroups of an XCD (S of them, slot = bid / 8) take its range in
-// rounds of S items, in alternating direction: round r gives slot s the
-// item r*S + s (even r) or r*S + S-1-s (odd r).  For causal items (heaviest
-// query tiles of a head first) this gives every slot about the same work
-// over each pair of rounds, and all the workgroups of an XCD work on the
-// same one or two heads at a time.  With one workgroup per item (grids that
-// fit at once, key splits) there is a single round.
-__device__ __forceinline__ int static_item(const Args &a, int bid, int grid, int r)
+// Persistent grid: workgroup bid's item of round r (-1 past the end of its
+// XCD's range).  The workgroups of an XCD (S of them, slot = bid / 8) take
+// its range in rounds of S items, in alternating direction: round r gives
+// slot s the item r*S + s (even r) or r*S + S-1-s (odd r).  For causal items
+// (heaviest query tiles of a head first) this gives every workgroup about
+// the same work over each pair of rounds, and all the workgroups of an XCD
+// work on the same one or two heads at a time.
+__device__ __forceinline__ int persistent_item(const Args &a, int bid, int grid, int r)
 {
     const int xcd = bid % NXCD, slot = bid / NXCD;
     const int S = (grid - xcd + NXCD - 1) / NXCD;
     const int i = r * S + ((r & 1) ? S - 1 - slot : slot);
     return i < xcd_range_n(a, xcd) ? xcd_range_lo(a, xcd) + i : -1;
+}
+
+// One workgroup per item: workgroup bid's item.  The hardware fills every CU
+// of an XCD with one workgroup (slots 0 .. R-1, R = CUs per XCD) before it
+// puts a second one on any (slots R .. 2R-1 again on CUs 0 .. R-1, and so
+// on), so the slots are dealt the XCD's items in rounds of R in alternating
+// direction: slot k and slot R + k, which share a CU, get a heavy and a
+// light causal query tile instead of two alike.
+__device__ __forceinline__ int static_item(const Args &a, int bid)
+{
+    const int xcd = bid % NXCD, slot = bid / NXCD;
+    const int n = xcd_range_n(a, xcd);
+    const int R = a.cu_per_xcd > 0 ? a.cu_per_xcd : n;
+    const int r = slot / R, p = slot % R;
+    const int m = min(R, n - r * R);   // slots of this round
+    return xcd_range_lo(a, xcd) + r * R + ((r & 1) ? m - 1 - p : p);
 }
 
 // One work item's coordinates and key-tile range (wave-uniform).
@@ -722,7 +738,7 @@ __global__ __launch_bounds__(NT, QW == 16 && D == 64 ? 4 : 2) void attn_fwd_kern
     k.half = k.lane / QW;
     k.off = a.Sk - a.Sq;
 
-    int L = static_item(a, blockIdx.x, gridDim.x, 0);
+    int L = PERSIST ? persistent_item(a, blockIdx.x, gridDim.x, 0) : static_item(a, blockIdx.x);
     if (L < 0)
         return;
     k.cur = k.describe(L);
@@ -741,7 +757,7 @@ __global__ __launch_bounds__(NT, QW == 16 && D == 64 ? 4 : 2) void attn_fwd_kern
 
     int st = 0;
     for (int r = 1;; ++r) {
-        L = PERSIST ? static_item(a, blockIdx.x, gridDim.x, r) : -1;
+        L = PERSIST ? persistent_item(a, blockIdx.x, gridDim.x, r) : -1;
         k.has_next = L >= 0;
         if (k.has_next)
             k.nxt = k.describe(L);
@@ -817,10 +833,14 @@ int grid_size(int n_items, int n_split, bool causal, int n_cu)
 // without a workgroup run as 64-query workgroups (16 query rows per wave)
 // instead: twice the workgroups, each wave's chain of key tiles half as long
 // in MFMA and softmax work (measured on one MI355X: B=1 H=32 S=512 causal
-// 134 -> 170 and non-causal 288 -> 340 TFLOP/s).  Where the 64-query grid
-// would put two workgroups on a CU it measured 2-9 % slower than the
-// 128-query grid (its waves read each K/V tile from LDS for half as many
-// queries), so larger grids keep 128-query tiles.
+// 134 -> 170 and non-causal 288 -> 340 TFLOP/s).  So do causal grids of at
+// most one 128-query workgroup per CU whose query tiles differ in cost by
+// more than a factor of two (Sk - Sq < Sq): their heavy and light 64-query
+// tiles pair up on the CUs (B=1 H=32 S=1024 causal 324 -> 370).  Where the
+// costs are even (non-causal, or a short query chunk against a long key
+// range) a 64-query grid with two workgroups per CU measured 7-9 % slower
+// than the 128-query grid (its waves read each K/V tile from LDS for half
+// as many queries).
 #ifndef TA_SMALL_TILES
 #define TA_SMALL_TILES 1
 #endif
@@ -965,11 +985,14 @@ ta_status attn_fwd_any(const void *Q, const void *K, const void *V, void *O, boo
 
     hipStream_t s = (hipStream_t)stream;
     const int n_cu = current_cu_count();
-    const bool small = TA_SMALL_TILES && n_split == 1 && n_cu > 0 && 2 * n_items <= (int64_t)n_cu;
+    const bool small = TA_SMALL_TILES && n_split == 1 && n_cu > 0 &&
+                       (2 * n_items <= (int64_t)n_cu ||
+                        (causal && Sk - Sq < Sq && n_items <= (int64_t)n_cu));
     if (small) {
         a.n_qt = (Sq + BM_SMALL - 1) / BM_SMALL;
         a.n_items = B * Hq * a.n_qt;
     }
+    a.cu_per_xcd = n_cu % NXCD == 0 ? n_cu / NXCD : 0;
     const int grid = small ? a.n_items : grid_size(a.n_items, n_split, causal != 0, n_cu);
     hipError_t e;
     const bool kb = o_bf16 && n_split == 1;   // the attention kernel writes bf16 O itself
