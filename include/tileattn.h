@@ -199,7 +199,7 @@ ta_status mla_decode(const void *Q, const void *Q_pe, const void *KV, const void
 ta_status mla_workspace_bytes(int B, int H, int num_splits, size_t *bytes);
 
 /* A split count for mla_decode: enough splits of the cache for one
- * workgroup per CU (a workgroup covers 64 query heads of one latent head and
+ * workgroup per CU (a workgroup covers 128 query heads of one latent head and
  * fills its CU's registers), keeping at least 8 tiles (256 positions) per
  * split.  No HIP call. */
 ta_status mla_split_heuristic(int B, int H, int Hkv, int Skv, int *num_splits);

@@ -10,29 +10,32 @@
 // cache serving again as the value).  The design is this library's own for
 // CDNA4:
 //
-//  * One workgroup of four wave64s (one per SIMD) owns HB = 64 query heads
-//    of one latent head of one batch element, and one range of cache tiles
-//    (a key split).  The waves form two pairs, each pair owning 32 heads.
-//    S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (A = 32 cache rows from LDS,
-//    B = the query of the pair's heads, held in registers for the whole
-//    kernel): the two waves of a pair each take half of the 576-wide
-//    contraction (18 of its 36 k-steps) and exchange their partial scores
-//    through LDS, so both hold the full scores of the tile.  In the
-//    accumulator layout lane l owns head l % 32, so the softmax row
-//    reductions are in-lane plus one v_permlane32_swap.
-//  * O^T += V^T P^T: the bf16 weights already sit in the B-operand layout;
-//    V^T comes from the same latent rows in LDS through the transpose read
-//    ds_read_b64_tr_b16.  Each wave of a pair accumulates half (256) of the
-//    512 output dims of its 32 heads: 128 fp32 registers per lane, kept in
-//    the matrix-core registers; LDS holds only the streamed cache tiles and
-//    the score exchange.
+//  * One workgroup of eight wave64s (two per SIMD) owns HB = 128 query
+//    heads of one latent head of one batch element, and one range of cache
+//    tiles (a key split); wave w owns 16 of the heads.  S^T = K Q^T with
+//    v_mfma_f32_16x16x32_bf16 over the full 576-wide contraction (A = 16
+//    cache rows from LDS, B = the query of the wave's 16 heads, held in
+//    registers for the whole kernel: 72 per lane).  In the 16x16 accumulator
+//    layout lane l owns head l % 16 and four positions of each 16-position
+//    block, so the softmax row reductions are in-lane plus two lane swaps
+//    (v_permlane32_swap, v_permlane16_swap).  No wave shares its scores or
+//    its softmax with another.
+//  * O^T += V^T P^T over all 512 output dims of the wave's heads (32 blocks
+//    of 16 dims, 128 fp32 registers per lane): the bf16 weights already sit
+//    in the B-operand layout (the MFMA's 32-position reduction order is
+//    chosen to match), and V^T comes from the same latent rows in LDS through
+//    the transpose read ds_read_b64_tr_b16.  The P V of tile j-1 is issued
+//    after the score MFMAs of tile j, so it overlaps tile j's softmax.
 //  * Cache tiles of 32 positions go global -> LDS by DMA (buffer_load_dwordx4
-//    ... lds) into a ring of four buffers, three tiles ahead of the one in
-//    use: the latent part [32][512] and the rotary part [32][64] in two
-//    regions.  16-byte chunks are XOR-swizzled so that the
-//    score operand reads (ds_read_b128) and the transpose reads of the same
-//    latent rows are both bank-conflict free (chunk c of latent row r at
-//    c ^ (((r & 3) << 2) | ((r >> 2) & 3)), of rotary row r at c ^ ((r >> 1) & 7)).
+//    ... lds) into a ring of four buffers, two tiles ahead of the one in
+//    use: the latent part [32][512] and the rotary part [32][64] of a tile
+//    side by side; one barrier per tile.  16-byte chunks are XOR-swizzled so
+//    that the score operand reads (ds_read_b128) and the transpose reads of
+//    the same latent rows are both bank-conflict free (chunk c of latent row
+//    r at c ^ (2 (r & 7) + ((r >> 3) & 1)) within its aligned group of 16,
+//    of rotary row r at c ^ ((r >> 1) & 7)): a score operand read touches
+//    rows 16b .. 16b + 15 at one chunk each, a transpose read rows 4g .. 4g + 3
+//    of two lane groups at two adjacent chunks each.
 //  * Online softmax as in the attention kernel: the running max m is raised
 //    when a head's tile max passes m + min(8, max(0, log2(l / 4))) (l the
 //    lane's running sum), so a position that could dominate a head is
@@ -45,6 +48,7 @@
 #include <stdint.h>
 
 #include "tileattn.h"
+#include "lds_dma.h"
 #include "split_combine.h"
 
 namespace {
@@ -62,25 +66,29 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 constexpr int DL = 512;              // latent width (query, cache, output)
 constexpr int DR = 64;               // rotary width (query, key)
 constexpr int BN = 32;               // cache positions per tile
-constexpr int NT = 256;              // threads per workgroup (4 waves)
-constexpr int HB = 64;               // query heads per workgroup (two wave pairs x 32)
-constexpr int KKL = DL / 16;         // MFMA k-steps over the latent part
-constexpr int KKR = DR / 16;         // ... over the rotary part
-constexpr int KKH = (KKL + KKR) / 2; // k-steps per wave of a pair
-constexpr int DH = DL / 2;           // output dims per wave
-constexpr int DBV = DH / 32;         // 32-row blocks of the wave's O^T
+constexpr int NW = 8;                // waves per workgroup (two per SIMD)
+constexpr int NT = 64 * NW;          // threads per workgroup
+constexpr int HW = 16;               // query heads per wave
+constexpr int HB = HW * NW;          // query heads per workgroup
+constexpr int KSL = DL / 32;         // MFMA k-steps (32 wide) over the latent part
+constexpr int KS = (DL + DR) / 32;   // ... over latent and rotary
+constexpr int DBO = DL / 16;         // 16-row blocks of a wave's O^T
 constexpr int LAT_BYTES = BN * DL * 2;
 constexpr int ROT_BYTES = BN * DR * 2;
-constexpr int LAT_PER_THREAD = BN * (DL / 8) / NT;   // 16-byte DMA chunks per thread
-constexpr int ROT_PER_THREAD = BN * (DR / 8) / NT;
+constexpr int STAGE_BYTES = LAT_BYTES + ROT_BYTES;
+constexpr int NST = 4;               // ring buffers
+constexpr int LAT_PER_THREAD = BN * (DL / 8) / NT;   // 16-byte latent DMA chunks per thread
+constexpr int ROT_THREADS = BN * (DR / 8);           // threads with one rotary chunk each
 constexpr int NXCD = 8;
 constexpr float LOG2E = 1.44269504088896340736f;
 constexpr float LN2 = 0.69314718055994530942f;
 constexpr float RESCALE_SLACK = 8.0f;       // base-2 headroom: weights never exceed 2^8
 constexpr float RAISE_SHARE_LOG2 = -2.0f;   // log2 of the share (1/4) of l a position may
                                             // weigh before the max is raised
-[[maybe_unused]] constexpr int BUF_RSRC_WORD3 = 0x00020000;
-static_assert(LAT_PER_THREAD == 8 && ROT_PER_THREAD == 1, "tile/thread mismatch");
+static_assert(KSL == 16 && KS == 18 && DBO == 32, "k-steps / output blocks");
+static_assert(LAT_PER_THREAD == 4 && ROT_THREADS == 256 && NT == 512, "tile/thread mismatch");
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct MArgs {
     const uint16_t *Q, *Qpe, *KV, *Kpe;
@@ -95,12 +103,12 @@ struct MArgs {
 };
 
 // 16-byte chunk swizzles (XOR within aligned groups of 16, resp. 8, chunks)
-__device__ __forceinline__ int lat_swz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+__device__ __forceinline__ int lat_swz(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
 __device__ __forceinline__ int rot_swz(int r) { return (r >> 1) & 7; }
 
-__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c)
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c)
 {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
@@ -108,297 +116,245 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
-__device__ __forceinline__ float max_halves(float x)
+// x over the four lanes l, l ^ 16, l ^ 32, l ^ 48 that hold one head
+__device__ __forceinline__ float max_head(float x)
 {
-    const u32x2 r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
-                                                     false, false);
+    u32x2 r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                               false);
+    x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
-__device__ __forceinline__ float sum_halves(float x)
+__device__ __forceinline__ float sum_head(float x)
 {
-    const u32x2 r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
-                                                     false, false);
+    u32x2 r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                               false);
+    x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Tile DMA is issued as inline assembly (buffer_load_dwordx4 ... lds), so
-// the compiler does not track it: it then never drains the tile loads in
-// flight before an LDS read (it cannot tell which buffer a DMA writes), and
-// the kernel waits for them itself with these vmcnt waits.  The kernel's
-// only other vector-memory operations are the query loads before the first
-// DMA and the output stores after the last wait.
-constexpr int DMA_PER_TILE = LAT_PER_THREAD + ROT_PER_THREAD;   // per thread
-static_assert(DMA_PER_TILE == 9, "vmcnt encodings below");
-// s_waitcnt vmcnt(n) (low 4 bits of n in [3:0], high 2 bits in [15:14]),
-// expcnt and lgkmcnt left at their maxima
-__device__ __forceinline__ void wait_dma_tiles_left(int tiles)   // tiles: 0, 1 or 2, uniform
+// Tile DMA is issued as inline assembly (lds_dma.h), so the compiler does
+// not track it: it never drains the tile loads in flight at a barrier, and
+// the kernel waits for them itself.  The kernel's only other vector-memory
+// operations are the query loads, waited for before the first tile, and the
+// output stores after the last tile.  Waves 0-3 issue one rotary chunk per
+// tile besides their latent chunks.
+template <int TILES_IN_FLIGHT>
+__device__ __forceinline__ void wait_tiles(bool rot_wave)
 {
-    if (tiles >= 2)
-        __builtin_amdgcn_s_waitcnt(0x4F72);   // vmcnt(18)
-    else if (tiles == 1)
-        __builtin_amdgcn_s_waitcnt(0x0F79);   // vmcnt(9)
+    if (rot_wave)
+        tileattn_dma::wait_vmcnt<TILES_IN_FLIGHT * (LAT_PER_THREAD + 1)>();
     else
-        __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+        tileattn_dma::wait_vmcnt<TILES_IN_FLIGHT * LAT_PER_THREAD>();
 }
-
-typedef uint32_t u32x4s __attribute__((ext_vector_type(4)));
-
-// A raw buffer resource (stride 0, 32-bit format, range-checked) in scalar
-// registers.
-__device__ __forceinline__ u32x4s buffer_rsrc(const void *base, uint32_t bytes)
-{
-    const uint64_t a = (uint64_t)(uintptr_t)base;
-    return u32x4s{(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a),
-                  (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32) & 0xFFFFu),
-                  (uint32_t)__builtin_amdgcn_readfirstlane(bytes), (uint32_t)BUF_RSRC_WORD3};
-}
-
-// One 16-byte-per-lane DMA: lane l's 16 bytes at byte `voff` of the buffer
-// land at LDS address `lds` + 16 l (`lds` wave-uniform).
-// M0 is an operand of the statement, so the compiler sets it (and keeps any
-// value of its own) around the load.
-__device__ __forceinline__ void dma16(uint32_t lds, uint32_t voff, u32x4s rsrc)
-{
-    asm volatile("s_nop 0\n\t"   // one wait state between the M0 write and the load
-                 "buffer_load_dwordx4 %0, %1, 0 offen lds"
-                 :
-                 : "v"(voff), "s"(rsrc), "{m0}"(__builtin_amdgcn_readfirstlane(lds))
-                 : "memory");
-}
-
-__device__ __forceinline__ uint32_t lds_addr(const void *p)
-{
-    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
-}
-
-// LDS exchange between the two waves of a pair: each wave's partial scores
-// (its half of the 576-wide dot products) in the accumulator layout, and at
-// the end nothing else (both waves then hold identical softmax state)
-struct Xchg {
-    float4 s[4][4][64];   // [wave][r / 4][lane]: 16-byte accesses, lanes contiguous
-};
 
 struct Mla {
     const MArgs &a;
-    int wave, lane, col, half;
-    int k_half;                     // which 18 of the 36 score k-steps this wave computes
-    int dim_half;                   // which 256 output dims this wave accumulates
+    int wave, lane, hc, gq;         // hc = lane % 16 (the head), gq = lane / 16
+    int wave_u;                     // the wave index, in a scalar register
+    bool rot_wave;                  // this wave also fetches rotary chunks
     const uint16_t *kv_b, *kpe_b;   // cache of (batch, latent head) at position 0
-    uint32_t lat_off[4], rot_off;   // per-lane DMA source offsets (see init_dma)
-    bf16x8 qreg[KKH];               // the query's k-steps 18 k_half .. +18
-    f32x16 acc_o[DBV];
+    uint32_t lat_off[2], rot_off;   // per-lane DMA source offsets (see init_lanes)
+    uint32_t ka[4], ra[2];          // per-lane LDS offsets of the score operands
+    uint32_t va[8];                 // ... of the value transpose reads
+    bf16x8 qreg[KS];                // the query of head hc: dims 32kk + 8gq .. +8
+    f32x4 acc_o[DBO];
     float m_run, l_run;
     float m_trig;   // the running max is raised when a tile max exceeds this
 
     __device__ Mla(const MArgs &args) : a(args) {}
 
-    // Latent DMA slot i*NT + 64w + l (i < 8) is row r = 4i + w, stored chunk
-    // sc = l, fetched from source chunk sc ^ lat_swz(r) = l ^ (w << 2) ^ (i & 3):
-    // four per-lane offsets (i & 3), plus 4(i & ~3) rows of pitch.  Rotary
-    // slot 64w + l is row 8w + l / 8, chunk l % 8, fetched from chunk
-    // (l % 8) ^ rot_swz(row).
-    __device__ __forceinline__ void init_dma()
+    // Latent DMA slot i*NT + 64w + l (i < 4) is row r = 8i + w, stored chunk
+    // l, fetched from source chunk l ^ lat_swz(r) = l ^ (2w + (i & 1)): two
+    // per-lane offsets (rows w and 8 + w) and a scalar 16 (i >> 1) rows of
+    // pitch address all four.  Rotary slot 64w + l (waves 0-3) is row
+    // 8w + l / 8, chunk l % 8, fetched from chunk (l % 8) ^ rot_swz(row).
+    //   Score operand of k-step kk, position block b (rows 16b + hc): latent
+    // chunk 4kk + gq at byte 256 (kk >> 2) + 16 ((4 (kk & 3) + gq) ^ lat_swz(hc))
+    // of the row, rotary chunk 4 (kk - 16) + gq at 16 ((4 (kk - 16) + gq) ^
+    // (hc >> 1)).
+    //   Value transpose reads: in each group of 16 lanes, lane 4i + c reads
+    // dims d0 + 4c .. +3 of row r0 + i, and lane j of the group then holds dim
+    // d0 + j of rows r0 .. r0 + 3.  Group gq reads rows 4gq .. (k-slots 0-3)
+    // and 16 + 4gq .. (k-slots 4-7, the same swizzle 16 KiB on); dims
+    // 16db .. of block db are chunk 2db + ((hc & 3) >> 1), byte 8 (hc & 1).
+    __device__ __forceinline__ void init_lanes()
     {
-        const int wave_u = __builtin_amdgcn_readfirstlane(wave);
         const uint32_t lat_pitch = (uint32_t)a.Hkv * DL * 2, rot_pitch = (uint32_t)a.Hkv * DR * 2;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            lat_off[i] = (4 * i + wave_u) * lat_pitch + 16 * (lane ^ (wave_u << 2) ^ i);
-        const int r = 8 * wave_u + lane / 8;
-        rot_off = r * rot_pitch + 16 * ((lane % 8) ^ rot_swz(r));
+        for (int p = 0; p < 2; ++p) {
+            const int r = 8 * p + wave_u;
+            lat_off[p] = r * lat_pitch + 16 * (lane ^ lat_swz(r));
+        }
+        const int rr = 8 * (wave_u & 3) + lane / 8;
+        rot_off = rr * rot_pitch + 16 * ((lane % 8) ^ rot_swz(rr));
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+            ka[m] = hc * (DL * 2) + 16 * ((4 * m + gq) ^ lat_swz(hc));
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+            ra[m] = LAT_BYTES + hc * (DR * 2) + 16 * ((4 * m + gq) ^ (hc >> 1));
+        const int row = 4 * gq + (hc >> 2);
+#pragma unroll
+        for (int m = 0; m < 8; ++m)
+            va[m] = row * (DL * 2) + 16 * ((2 * m + ((hc & 3) >> 1)) ^ lat_swz(row)) + 8 * (hc & 1);
     }
 
-    // DMA cache tile j (positions j*BN ..) into the latent and rotary
-    // buffers.  Each buffer resource starts at the tile and ends after its
-    // last valid row; a row past Skv re-reads the last valid row (its scores
-    // are masked), so no lane addresses outside the cache.
-    __device__ __forceinline__ void dma_tile(int j, unsigned char *lat, unsigned char *rot) const
+    // DMA cache tile j (positions j*BN ..) into `stage`.  Each buffer
+    // resource starts at the tile and ends after its last valid row; a row
+    // past Skv re-reads the last valid row (its scores are masked and its
+    // weights zero), so no lane addresses outside the cache.
+    __device__ __forceinline__ void dma_tile(int j, unsigned char *stage) const
     {
         const int valid = min(BN, a.Skv - j * BN);
         const size_t row0 = (size_t)j * BN * a.Hkv;
         const uint32_t lat_pitch = (uint32_t)a.Hkv * DL * 2, rot_pitch = (uint32_t)a.Hkv * DR * 2;
-        const u32x4s rl = buffer_rsrc(kv_b + row0 * DL, (valid - 1) * lat_pitch + DL * 2);
-        const u32x4s rr = buffer_rsrc(kpe_b + row0 * DR, (valid - 1) * rot_pitch + DR * 2);
-        const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-        const int last = valid - 1;
-        const uint32_t lat_base = lds_addr(lat), rot_base = lds_addr(rot);
+        const tileattn_dma::u32x4s rl =
+            tileattn_dma::buffer_rsrc(kv_b + row0 * DL, (valid - 1) * lat_pitch + DL * 2);
+        const uint32_t lat_base = tileattn_dma::lds_addr(stage) + wave_u * 64 * 16;
+        if (valid == BN) {
 #pragma unroll
-        for (int i = 0; i < LAT_PER_THREAD; ++i) {
-            // row 4i + w, or the last valid row past it; lat_off[i & 3] holds
-            // row 4(i & 3) + w.  (The difference can be negative: it is added
-            // to the vector offset modulo 2^32.)
-            const int row = 4 * i + wave_u;
-            const int src = row > last ? last : row;
-            const uint32_t o =
-                lat_off[i & 3] + (uint32_t)((src - 4 * (i & 3) - wave_u) * (int)lat_pitch);
-            dma16(lat_base + (i * NT + wave_u * 64) * 16, o, rl);
+            for (int i = 0; i < LAT_PER_THREAD; ++i)
+                tileattn_dma::dma16_soff(lat_base + i * NT * 16, lat_off[i & 1],
+                                         16 * (i >> 1) * lat_pitch, rl);
+        } else {
+            const int last = valid - 1;
+#pragma unroll
+            for (int i = 0; i < LAT_PER_THREAD; ++i) {
+                // row 8i + w, or the last valid row past it (the difference,
+                // possibly negative, is added modulo 2^32)
+                const int row = 8 * i + wave_u;
+                const int src = row > last ? last : row;
+                const uint32_t o = lat_off[i & 1] + (uint32_t)((src - 8 * (i & 1) - wave_u) *
+                                                               (int)lat_pitch);
+                tileattn_dma::dma16(lat_base + i * NT * 16, o, rl);
+            }
         }
-        {
+        if (rot_wave) {
+            const tileattn_dma::u32x4s rr =
+                tileattn_dma::buffer_rsrc(kpe_b + row0 * DR, (valid - 1) * rot_pitch + DR * 2);
             // row 8w + l/8 is lane-dependent: clamp per lane
-            const int row = 8 * wave_u + lane / 8;
-            const int shift = row > last ? row - last : 0;
-            dma16(rot_base + wave_u * 64 * 16, rot_off - (uint32_t)shift * rot_pitch, rr);
+            const int row = 8 * (wave_u & 3) + lane / 8;
+            const int shift = row > valid - 1 ? row - (valid - 1) : 0;
+            tileattn_dma::dma16(tileattn_dma::lds_addr(stage + LAT_BYTES) + wave_u * 64 * 16,
+                                rot_off - (uint32_t)shift * rot_pitch, rr);
         }
     }
 
-    // Partial S^T[position][head] over this wave's 18 k-steps (288 of the
-    // 576 key dims) for the tile's 32 positions; k-step kk < 32 is latent
-    // chunk 2kk + half, kk >= 32 rotary chunk 2(kk - 32) + half.  Two
-    // interleaved accumulation chains.
-    template <int KH>
-    __device__ __forceinline__ void scores(const unsigned char *lat, const unsigned char *rot,
-                                           f32x16 &s) const
+    // S^T[position][head] of the tile's two 16-position blocks, each as two
+    // interleaved accumulation chains over the 18 k-steps
+    __device__ __forceinline__ void scores(const unsigned char *stage, f32x4 (&s)[2]) const
     {
-        f32x16 s0, s1;
+        f32x4 c[2][2];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            s0[r] = 0.f;
-            s1[r] = 0.f;
-        }
-        const int row = col;
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
-        for (int i = 0; i < KKH; ++i) {
-            const int kk = KH * KKH + i;
-            bf16x8 av;
-            if (kk < KKL)   // byte 256 (kk >> 3) + 16 ((2 (kk & 7) + half) ^ lat_swz(row))
-                av = *(const bf16x8 *)(lat + row * (DL * 2) + 256 * (kk >> 3) +
-                                       16 * ((2 * (kk & 7) + half) ^ lat_swz(row)));
-            else
-                av = *(const bf16x8 *)(rot + row * (DR * 2) +
-                                       16 * ((2 * (kk - KKL) + half) ^ rot_swz(row)));
-            if (i & 1)
-                s1 = mfma32(av, qreg[i], s1);
-            else
-                s0 = mfma32(av, qreg[i], s0);
-            if ((i & 7) == 7)   // bound how far ahead operand reads are issued
-                __builtin_amdgcn_sched_barrier(0);
-        }
-        s = s0 + s1;
-    }
-
-    // O^T += V^T P^T for one tile: the weights pk (B-operand layout) of its
-    // 32 positions and the transpose reads of its latent rows for this
-    // wave's 256 output dims
-    __device__ __forceinline__ void pv(const uint32_t (&pk)[8], const unsigned char *lat)
-    {
-        // MFMA k-slot t of half h stands for position 16ks + 4h + t (t < 4)
-        // or 16ks + 8 + 4h + t-4, matching where the accumulator left P
-        const int gq = lane >> 4, sl = lane & 15;
-        const int c = 2 * (gq & 1) + ((sl & 3) >> 1);
-        const int byte_in = 8 * (sl & 1);
+            for (int h = 0; h < 2; ++h)
+                c[b][h] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < BN / 16; ++ks) {
-            const u32x4 bw = {pk[4 * ks], pk[4 * ks + 1], pk[4 * ks + 2], pk[4 * ks + 3]};
-            const bf16x8 bv = __builtin_bit_cast(bf16x8, bw);
-            const int row0 = 16 * ks + 4 * half + (sl >> 2);
-            const int row1 = row0 + 8;
-            // dims d = 256 dim_half + 32db + 16(gq & 1) + 4(sl & 3): chunk
-            // d >> 3 = 32 dim_half + 4db + c, XOR-swizzled within its group of
-            // 16: byte 512 dim_half + 256 (db >> 2) + 16 ((4(db & 3) + c) ^ f)
-            const unsigned char *r0 = lat + row0 * (DL * 2) + 512 * dim_half + byte_in;
-            const unsigned char *r1 = lat + row1 * (DL * 2) + 512 * dim_half + byte_in;
-            const int f0 = lat_swz(row0), f1 = lat_swz(row1);
+        for (int kk = 0; kk < KS; ++kk)
 #pragma unroll
-            for (int db = 0; db < DBV; ++db) {
-                const unsigned char *p0 = r0 + 256 * (db >> 2) + 16 * ((4 * (db & 3) + c) ^ f0);
-                const unsigned char *p1 = r1 + 256 * (db >> 2) + 16 * ((4 * (db & 3) + c) ^ f1);
-                const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p0);
-                const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p1);
-                const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
-                const u32x4 aw = {l2[0], l2[1], h2[0], h2[1]};
-                acc_o[db] = mfma32(__builtin_bit_cast(bf16x8, aw), bv, acc_o[db]);
+            for (int b = 0; b < 2; ++b) {
+                const unsigned char *p =
+                    kk < KSL ? stage + ka[kk & 3] + 256 * (kk >> 2) + 16 * (DL * 2) * b
+                             : stage + ra[kk - KSL] + 16 * (DR * 2) * b;
+                const bf16x8 av = *(const bf16x8 *)p;
+                c[b][kk & 1] = mfma16(av, qreg[kk], c[b][kk & 1]);
             }
-            __builtin_amdgcn_sched_barrier(0);
+        s[0] = c[0][0] + c[0][1];
+        s[1] = c[1][0] + c[1][1];
+    }
+
+    // O^T += V^T P^T for one tile: the weights pk (B-operand layout: k-slot t
+    // of lane group gq is position 4gq + t for t < 4, 16 + 4gq + t - 4 after)
+    // and the transpose reads of the tile's latent rows, all 512 dims
+    __device__ __forceinline__ void pv(const uint32_t (&pk)[4], const unsigned char *stage)
+    {
+        const bf16x8 bv = __builtin_bit_cast(bf16x8, u32x4{pk[0], pk[1], pk[2], pk[3]});
+#pragma unroll
+        for (int db = 0; db < DBO; ++db) {
+            const unsigned char *p = stage + va[db & 7] + 256 * (db >> 3);
+            const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p);
+            const i16x4 hi =
+                __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(p + 16 * (DL * 2)));
+            const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+            const u32x4 aw = {l2[0], l2[1], h2[0], h2[1]};
+            acc_o[db] = mfma16(__builtin_bit_cast(bf16x8, aw), bv, acc_o[db]);
         }
     }
 
-    // One cache tile j, software-pipelined one tile deep: the partial
-    // scores of tile j, then the P V of tile j-1 (its weights pk from the
-    // previous step, its rows still in the previous buffer) while the
-    // partial scores travel to the partner wave; after the barrier, tile
-    // j+3 goes into that previous buffer, and the softmax of tile j leaves
-    // its weights in pk for the next step.  KH = k_half, a template argument
-    // so that the query's k-steps are indexed statically.
-    template <bool MASKED, int KH, bool PREV>
-    __device__ __forceinline__ void step(int j, int j_hi, const unsigned char *lat,
-                                         const unsigned char *rot, unsigned char *lat_p,
-                                         unsigned char *rot_p, uint32_t (&pk)[8], Xchg &x)
+    // Online softmax of tile j: mask, running max, weights into pk
+    template <bool MASKED>
+    __device__ __forceinline__ void softmax(int j, f32x4 (&s)[2], uint32_t (&pk)[4])
     {
-        f32x16 s;
-        scores<KH>(lat, rot, s);
-#pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4)
-            x.s[wave][r4][lane] = float4{s[4 * r4], s[4 * r4 + 1], s[4 * r4 + 2], s[4 * r4 + 3]};
-        if (PREV)
-            pv(pk, lat_p);
-        __syncthreads();
-        // every wave is past tile j-1 now: its buffers take tile j+3
-        if (j + 3 < j_hi)
-            dma_tile(j + 3, lat_p, rot_p);
-        // (k-half 0) + (k-half 1) in the same order on both waves, so that
-        // the pair computes bitwise the same scores
-#pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-            const float4 o = x.s[wave ^ 1][r4][lane];
-            const float ov[4] = {o.x, o.y, o.z, o.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int r = 4 * r4 + e;
-                s[r] = KH == 0 ? s[r] + ov[e] : ov[e] + s[r];
-            }
-        }
-
-        // lane holds positions j*BN + 8(r/4) + 4half + r%4 of head col
+        // lane holds positions j*BN + 16b + 4gq + r of head hc
         float mx = -INFINITY;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            if (MASKED) {
-                const int pos = j * BN + 8 * (r >> 2) + 4 * half + (r & 3);
-                s[r] = pos < a.Skv ? s[r] : -INFINITY;
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                if (MASKED) {
+                    const int pos = j * BN + 16 * b + 4 * gq + r;
+                    s[b][r] = pos < a.Skv ? s[b][r] : -INFINITY;
+                }
+                mx = fmaxf(mx, s[b][r]);
             }
-            mx = fmaxf(mx, s[r]);
-        }
-        mx = max_halves(mx);
+        mx = max_head(mx);
         const float m_tile = mx * a.c;   // every tile holds a valid position
         if (__builtin_amdgcn_ballot_w64(m_tile > m_trig)) {
-            // acc already holds tile j-1, weighted with the old maximum
+            // acc holds the tiles before j (once their MFMAs are done),
+            // weighted with the old maximum
             const float m_new = fmaxf(m_run, m_tile);
             const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
             m_run = m_new;
             l_run *= alpha;
-            // block by block through vector registers: the accumulator
-            // stays in the matrix-core registers everywhere else
 #pragma unroll
-            for (int db = 0; db < DBV; ++db) {
-                f32x16 t = acc_o[db];
-                asm volatile("" : "+v"(t));
-                t *= alpha;
-                asm volatile("" : "+v"(t));
-                acc_o[db] = t;
-                asm volatile("" : "+a"(acc_o[db]));
-            }
+            for (int db = 0; db < DBO; ++db)
+                acc_o[db] *= alpha;
         }
         float rowsum = 0.f;
 #pragma unroll
-        for (int r = 0; r < 16; r += 2) {
-            float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], a.c, -m_run));
-            float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r + 1], a.c, -m_run));
-            if (MASKED) {
-                p0 = s[r] == -INFINITY ? 0.f : p0;
-                p1 = s[r + 1] == -INFINITY ? 0.f : p1;
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int r = 0; r < 4; r += 2) {
+                float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][r], a.c, -m_run));
+                float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][r + 1], a.c, -m_run));
+                if (MASKED) {
+                    p0 = s[b][r] == -INFINITY ? 0.f : p0;
+                    p1 = s[b][r + 1] == -INFINITY ? 0.f : p1;
+                }
+                rowsum += p0 + p1;
+                pk[2 * b + (r >> 1)] = pack_bf16(p0, p1);
             }
-            rowsum += p0 + p1;
-            pk[r >> 1] = pack_bf16(p0, p1);
-        }
         l_run += rowsum;
         // the level for the next tile (l = 0 gives m itself)
         m_trig = m_run + fminf(RESCALE_SLACK,
                                fmaxf(0.f, RAISE_SHARE_LOG2 + __builtin_amdgcn_logf(l_run)));
+    }
 
-        // tile j+1 must have landed (tiles j+2 and j+3 may stay in flight)
-        wait_dma_tiles_left(min(2, max(0, j_hi - 1 - (j + 1))));
+    // Tile t (counted from the split's first, key tile j = j_lo + t) in
+    // stage t % 4: once it has landed and every wave is past tile t-1, tile
+    // t+2 goes into the stage of tile t-2; then the scores of tile t, the
+    // P V of tile t-1 (weights pk, rows in stage (t-1) % 4) and the softmax
+    // of tile t, whose weights replace pk.
+    template <bool MASKED>
+    __device__ __forceinline__ void step(int t, int n, int j_lo, unsigned char *ring,
+                                         uint32_t (&pk)[4])
+    {
+        if (t + 1 < n)
+            wait_tiles<1>(rot_wave);
+        else
+            wait_tiles<0>(rot_wave);
         __syncthreads();
+        if (t + 2 < n)
+            dma_tile(j_lo + t + 2, ring + ((t + 2) % NST) * STAGE_BYTES);
+        f32x4 s[2];
+        scores(ring + (t % NST) * STAGE_BYTES, s);
+        if (t > 0)
+            pv(pk, ring + ((t + NST - 1) % NST) * STAGE_BYTES);
+        softmax<MASKED>(j_lo + t, s, pk);
     }
 };
 
@@ -419,168 +375,87 @@ __device__ __forceinline__ void decode_wg(const MArgs &a, int bid, int &b, int &
     b = l / a.Hkv;
 }
 
-// The tile loop of one wave, KH = its k-half (wave-uniform).  Four
-// buffers in a ring: tile j lives in buffer (j - j_lo) % 4; tile j+3 goes
-// into the buffer of tile j-1 once every wave has done that tile's P V.  The
-// ring is unrolled by four so that every buffer reference is static; the
-// last tile's P V follows the loop.
-template <int KH>
-__device__ __forceinline__ void run_tiles(Mla &k, int j_lo, int j_hi, int j_full,
-                                          unsigned char *const (&lat)[4],
-                                          unsigned char *const (&rot)[4], Xchg &xchg)
-{
-    uint32_t pk[8];
-    int j = j_lo;
-    // first tile: nothing before it to multiply into the output
-    if (j < j_full)
-        k.template step<false, KH, false>(j, j_hi, lat[0], rot[0], lat[3], rot[3], pk, xchg);
-    else
-        k.template step<true, KH, false>(j, j_hi, lat[0], rot[0], lat[3], rot[3], pk, xchg);
-    ++j;
-    int u = 1;   // buffer of tile j
-    if (j + 2 < j_full) {
-        for (; j + 3 < j_full; j += 4) {
-            k.template step<false, KH, true>(j, j_hi, lat[1], rot[1], lat[0], rot[0], pk, xchg);
-            k.template step<false, KH, true>(j + 1, j_hi, lat[2], rot[2], lat[1], rot[1], pk, xchg);
-            k.template step<false, KH, true>(j + 2, j_hi, lat[3], rot[3], lat[2], rot[2], pk, xchg);
-            k.template step<false, KH, true>(j + 3, j_hi, lat[0], rot[0], lat[3], rot[3], pk, xchg);
-        }
-    }
-    // at most three full tiles and a ragged one remain; tile j is in buffer
-    // (j - j_lo) % 4
-    u = (j - j_lo) & 3;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        if (j >= j_hi)
-            break;
-        // (buffers indexed at run time here: these remaining tiles are few)
-        switch (u) {
-#define TA_MLA_STEP(U)                                                                          \
-    case U:                                                                                     \
-        if (j < j_full)                                                                         \
-            k.template step<false, KH, true>(j, j_hi, lat[U], rot[U], lat[(U + 3) % 4],          \
-                                             rot[(U + 3) % 4], pk, xchg);                        \
-        else                                                                                    \
-            k.template step<true, KH, true>(j, j_hi, lat[U], rot[U], lat[(U + 3) % 4],           \
-                                            rot[(U + 3) % 4], pk, xchg);                         \
-        break;
-            TA_MLA_STEP(0)
-            TA_MLA_STEP(1)
-            TA_MLA_STEP(2)
-            TA_MLA_STEP(3)
-#undef TA_MLA_STEP
-        }
-        ++j;
-        u = (u + 1) & 3;
-    }
-    // the last tile's P V (its buffer is that of tile j_hi - 1)
-    switch ((j_hi - 1 - j_lo) & 3) {
-    case 0: k.pv(pk, lat[0]); break;
-    case 1: k.pv(pk, lat[1]); break;
-    case 2: k.pv(pk, lat[2]); break;
-    default: k.pv(pk, lat[3]); break;
-    }
-}
-
 __global__ __launch_bounds__(NT, 1) void mla_decode_kernel(MArgs args)
 {
-    __shared__ __attribute__((aligned(16))) unsigned char lat0[LAT_BYTES];
-    __shared__ __attribute__((aligned(16))) unsigned char lat1[LAT_BYTES];
-    __shared__ __attribute__((aligned(16))) unsigned char lat2[LAT_BYTES];
-    __shared__ __attribute__((aligned(16))) unsigned char lat3[LAT_BYTES];
-    __shared__ __attribute__((aligned(16))) unsigned char rot0[ROT_BYTES];
-    __shared__ __attribute__((aligned(16))) unsigned char rot1[ROT_BYTES];
-    __shared__ __attribute__((aligned(16))) unsigned char rot2[ROT_BYTES];
-    __shared__ __attribute__((aligned(16))) unsigned char rot3[ROT_BYTES];
-    __shared__ Xchg xchg;
+    __shared__ __attribute__((aligned(16))) unsigned char ring[NST * STAGE_BYTES];
 
     Mla k(args);
     const MArgs &a = args;
     const int tid = threadIdx.x;
     k.wave = tid >> 6;
     k.lane = tid & 63;
-    k.col = k.lane & 31;
-    k.half = k.lane >> 5;
-    k.k_half = k.wave & 1;
-    k.dim_half = k.wave & 1;
+    k.hc = k.lane & 15;
+    k.gq = k.lane >> 4;
+    k.wave_u = __builtin_amdgcn_readfirstlane(k.wave);
+    k.rot_wave = k.wave_u < ROT_THREADS / 64;
 
     int b, hk, hblk, split;
     decode_wg(a, blockIdx.x, b, hk, hblk, split);
     const int n_tiles = (a.Skv + BN - 1) / BN;
     const int j_lo = split * a.split_tiles;
     const int j_hi = min(n_tiles, j_lo + a.split_tiles);   // non-empty: splits cover the tiles
+    const int n = j_hi - j_lo;
 
-    // this lane's head: local index within the latent head's group (the
-    // pair of waves 2p, 2p+1 shares heads 32p .. 32p+31 of the block)
-    const int h_loc = hblk * HB + (k.wave >> 1) * 32 + k.col;
+    // this lane's head: local index within the latent head's group
+    const int h_loc = hblk * HB + k.wave_u * HW + k.hc;
     const bool head_ok = h_loc < a.g;
     const int head = hk * a.g + min(h_loc, a.g - 1);
 
     k.kv_b = a.KV + ((size_t)b * a.Skv * a.Hkv + hk) * DL;
     k.kpe_b = a.Kpe + ((size_t)b * a.Skv * a.Hkv + hk) * DR;
-    k.init_dma();
+    k.init_lanes();
 
-    // this wave's half of the query of the lane's head as the B operand:
-    // k-step kk holds dims 16kk + 8half .. +8 of [q | q_pe]
+    // prologue: the first two tiles in flight
+    k.dma_tile(j_lo, ring);
+    if (n > 1)
+        k.dma_tile(j_lo + 1, ring + STAGE_BYTES);
+
+    // the query of the lane's head as the B operand: k-step kk holds dims
+    // 32kk + 8gq .. +8 of [q | q_pe]
     {
-        const uint16_t *qp = a.Q + ((size_t)b * a.H + head) * DL + 8 * k.half;
-        const uint16_t *qr = a.Qpe + ((size_t)b * a.H + head) * DR + 8 * k.half;
+        const uint16_t *qp = a.Q + ((size_t)b * a.H + head) * DL + 8 * k.gq;
+        const uint16_t *qr = a.Qpe + ((size_t)b * a.H + head) * DR + 8 * k.gq;
 #pragma unroll
-        for (int i = 0; i < KKH; ++i) {
-            const int kk = k.k_half * KKH + i;
-            u32x4 v = kk < KKL ? *(const u32x4 *)(qp + 16 * kk)
-                               : *(const u32x4 *)(qr + 16 * (kk - KKL));
+        for (int kk = 0; kk < KS; ++kk) {
+            u32x4 v = kk < KSL ? *(const u32x4 *)(qp + 32 * kk)
+                               : *(const u32x4 *)(qr + 32 * (kk - KSL));
             if (!head_ok)
                 v = u32x4{0u, 0u, 0u, 0u};
-            k.qreg[i] = __builtin_bit_cast(bf16x8, v);
+            k.qreg[kk] = __builtin_bit_cast(bf16x8, v);
         }
     }
 #pragma unroll
-    for (int db = 0; db < DBV; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-            k.acc_o[db][r] = 0.f;
+    for (int db = 0; db < DBO; ++db)
+        k.acc_o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
     k.m_run = -INFINITY;
     k.l_run = 0.f;
     k.m_trig = -INFINITY;
-
-    // prologue: tiles j_lo .. j_lo+2 in flight, wait for the first
-    k.dma_tile(j_lo, lat0, rot0);
-    if (j_lo + 1 < j_hi)
-        k.dma_tile(j_lo + 1, lat1, rot1);
-    if (j_lo + 2 < j_hi)
-        k.dma_tile(j_lo + 2, lat2, rot2);
-    wait_dma_tiles_left(min(2, j_hi - 1 - j_lo));
-    __syncthreads();
+    // the query (issued after the prologue tiles; the tiles are waited for
+    // by the first step)
+    tileattn_dma::wait_vmcnt<0>();
 
     // every tile but a ragged last one is fully valid
-    const int j_full = min(j_hi, a.Skv / BN);
-    unsigned char *const lat[4] = {lat0, lat1, lat2, lat3};
-    unsigned char *const rot[4] = {rot0, rot1, rot2, rot3};
-    if (k.k_half)
-        run_tiles<1>(k, j_lo, j_hi, j_full, lat, rot, xchg);
-    else
-        run_tiles<0>(k, j_lo, j_hi, j_full, lat, rot, xchg);
+    const int n_full = min(j_hi, a.Skv / BN) - j_lo;
+    uint32_t pk[4];
+    int t = 0;
+    for (; t < n_full; ++t)
+        k.step<false>(t, n, j_lo, ring, pk);
+    if (t < n)
+        k.step<true>(t, n, j_lo, ring, pk);
+    // the last tile's P V
+    k.pv(pk, ring + ((n - 1) % NST) * STAGE_BYTES);
 
-    // epilogue: normalise and store this wave's 256 dims of the split's
-    // result for the lane's head (both waves of the pair hold the same sums)
-    const float l = sum_halves(k.l_run);
+    // epilogue: normalise and store the split's result of the lane's head:
+    // block db, lane group gq holds dims 16db + 4gq .. +3
+    const float l = sum_head(k.l_run);
     if (head_ok) {
         const float inv = 1.f / l;
         const size_t row = (size_t)b * a.H + head;
-        float *op = a.O + (size_t)split * a.o_split + row * DL + DH * k.dim_half;
+        float *op = a.O + (size_t)split * a.o_split + row * DL + 4 * k.gq;
 #pragma unroll
-        for (int db = 0; db < DBV; ++db)
-#pragma unroll
-            for (int gr = 0; gr < 4; ++gr) {
-                float4 v;
-                v.x = k.acc_o[db][4 * gr + 0] * inv;
-                v.y = k.acc_o[db][4 * gr + 1] * inv;
-                v.z = k.acc_o[db][4 * gr + 2] * inv;
-                v.w = k.acc_o[db][4 * gr + 3] * inv;
-                *(float4 *)(op + 32 * db + 8 * gr + 4 * k.half) = v;
-            }
-        if (k.half == 0 && k.dim_half == 0)
+        for (int db = 0; db < DBO; ++db)
+            *(f32x4 *)(op + 16 * db) = k.acc_o[db] * inv;
+        if (k.gq == 0)
             a.LSE[(size_t)split * a.l_split + row] = (k.m_run + log2f(l)) * LN2;
     }
 }

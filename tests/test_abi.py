@@ -231,7 +231,7 @@ def test_mla_workspace_and_heuristic():
     for B, H, Hkv, Skv in [(64, 128, 1, 8192), (128, 128, 1, 4096), (1, 128, 1, 64),
                            (2, 128, 1, 200), (8, 64, 2, 2048), (512, 128, 1, 4096)]:
         n = ta.mla_split_heuristic(B, H, Hkv, Skv)
-        wg = B * Hkv * -(-(H // Hkv) // 64)
+        wg = B * Hkv * -(-(H // Hkv) // 128)   # 128 query heads per workgroup
         tiles = -(-Skv // 32)
         assert 1 <= n <= 128
         if wg >= 256:

@@ -57,11 +57,11 @@ def test_mla_tiny_full_compare(ta, splits):
 EDGE = [
     # (B, H, Hkv, Skv, splits)
     (1, 128, 1, 1, 1), (2, 128, 1, 31, 1), (1, 128, 1, 32, 1), (1, 128, 1, 33, 2),
-    (3, 16, 1, 65, 1),       # 16 heads: the second wave pair idles, half a pair is padding
-    (2, 100, 1, 300, 4),     # 100 heads: two head blocks, the second partly padding
+    (3, 16, 1, 65, 1),       # 16 heads: one wave's worth, the other seven waves are padding
+    (2, 100, 1, 300, 4),     # 100 heads: one head block, a wave partly and one wholly padding
     (2, 64, 2, 257, 3),      # two latent heads of 32 query heads each
     (1, 128, 1, 1000, 128),  # more splits than tiles
-    (1, 256, 1, 96, 2),      # 256 heads: four head blocks
+    (1, 256, 1, 96, 2),      # 256 heads: two head blocks
 ]
 
 
