@@ -6,8 +6,12 @@
 //
 //  * One workgroup of eight wave64s computes a BM x BN tile of C (256 x 256,
 //    or 128 x 128 when the grid of large tiles would not fill the GPU); the
-//    waves form a 2 x 4 grid, each owning (BM/2) x (BN/4) as 32 x 32 blocks
-//    of v_mfma_f32_32x32x16_bf16 accumulators (fp32).  Two waves share each
+//    waves form a 2 x 4 grid, each owning (BM/2) x (BN/4) as 16 x 16 blocks
+//    of v_mfma_f32_16x16x32_bf16 accumulators (fp32; 32 x 32 blocks of
+//    v_mfma_f32_32x32x16_bf16 where four wave groups split each K step, see
+//    below).  Under the board's power limit the 16 x 16 x 32 form sustains
+//    a higher clock for the same work (random data, MFMAs alone: 2.15
+//    against 1.84 GHz, 2.18-2.26 against 1.72 PFLOP/s).  Two waves share each
 //    SIMD, so one's matrix-core work covers the other's LDS reads and
 //    barrier waits.  Four waves of 128 x 128 each read a third less from LDS
 //    per flop and run at a ~6 % higher clock under the board's power limit,
@@ -23,12 +27,14 @@
 //    k+1 runs under the MFMAs of step k.  With one workgroup per CU (small
 //    grids of 128 x 128 tiles) a ring of four stages keeps three steps in
 //    flight instead.
-//  * A operands (32 rows x 8 consecutive k per lane) are ds_read_b128 from
-//    the A tile, 16-byte chunk c of row r stored at c ^ ((r >> 1) & 7).  B
-//    operands (8 consecutive k of one column per lane) come from the
+//  * A operands (16 or 32 rows x 8 consecutive k per lane) are ds_read_b128
+//    from the A tile, 16-byte chunk c of row r stored at c ^ ((r >> 1) & 7).
+//    B operands (8 consecutive k of one column per lane) come from the
 //    row-major B tile through the transpose read ds_read_b64_tr_b16, chunk c
-//    of row r stored at c ^ 4 (r & 3).  Both swizzles make the operand reads
-//    bank-conflict free.
+//    of row r stored at c ^ (2 (r & 3) + 8 ((r >> 3) & 1)) for 16 x 16
+//    blocks (a half wave reads eight rows of 32 bytes) or c ^ 4 (r & 3) for
+//    32 x 32 ones (four rows of 64 bytes).  The swizzles keep the operand
+//    reads bank-conflict free.
 //  * The grid maps workgroups so that each XCD gets a contiguous range of
 //    tiles, taken in groups of four tile rows (column by column inside a
 //    group), so the tiles resident on one XCD form a 4 x 8 block that shares
@@ -44,6 +50,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -64,9 +71,14 @@ struct GArgs {
     int n_wg;
 };
 
-__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c)
+[[maybe_unused]] __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c)
 {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+[[maybe_unused]] __device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
@@ -110,17 +122,26 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p)
 }
 
 __device__ __forceinline__ int a_swz(int r) { return (r >> 1) & 7; }
-__device__ __forceinline__ int b_swz(int r) { return 4 * (r & 3); }
+// B swizzle for the transpose reads of MF x MF blocks: MF = 32 reads four
+// rows of 64 bytes per half wave, MF = 16 eight rows (4gq .. +3 of two lane
+// groups, 8 apart) of 32 bytes, whose chunk pairs it keeps apart
+template <int MF>
+__device__ __forceinline__ int b_swz(int r)
+{
+    return MF == 32 ? 4 * (r & 3) : 2 * (r & 3) + 8 * ((r >> 3) & 1);
+}
 
 // KS = 1: the eight waves tile C as 2 x 4.  KS = 2 or 4: KS groups of 8 / KS
 // waves, each group tiling C as 1 x (8 / KS) for its share of every K step
 // (a wave then reads less of the tiles per flop, most of all of B through
 // the transpose read); the groups' sums are added in LDS at the end.
-template <int BM, int BN, int KS = 1>
+template <int BM, int BN, int KS, int MF>
 struct Cfg {
     static constexpr int WPG = 8 / KS;                               // waves per group
     static constexpr int WM = KS == 1 ? BM / 2 : BM, WN = KS == 1 ? BN / 4 : BN / WPG;
-    static constexpr int FM = WM / 32, FN = WN / 32;      // 32 x 32 blocks per wave
+    static constexpr int FM = WM / MF, FN = WN / MF;      // MF x MF blocks per wave
+    static constexpr int AR = MF * MF / 64;               // accumulator values per lane and block
+    static constexpr int KW = 512 / MF;                   // k per MFMA (16 or 32)
     static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BK * BN * 2;
     static constexpr int A_PER_THREAD = BM * (BK / 8) / NT;   // 16-byte slots
     static constexpr int B_PER_THREAD = BK * (BN / 8) / NT;
@@ -132,14 +153,17 @@ struct Cfg {
 // flight during the MFMAs) or a ring of three or four (ST - 1 tiles in
 // flight) for grids of at most one workgroup per CU, where no other
 // workgroup's MFMAs cover the wait for a tile.
-template <int BM, int BN, int ST, int KS, bool CBF16>
+template <int BM, int BN, int ST, int KS, int MF, bool CBF16>
 __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
 {
-    using C = Cfg<BM, BN, KS>;
+    using C = Cfg<BM, BN, KS, MF>;
+    using Acc = typename std::conditional<MF == 32, f32x16, f32x4>::type;
     static_assert(KS == 1 || ((KS == 2 || KS == 4) && C::A_BYTES == 16384 &&
-                              C::B_BYTES == 16384 && C::FM * C::FN * 4096 * C::WPG == 65536),
+                              C::B_BYTES == 16384 &&
+                              C::FM * C::FN * C::AR * 256 * C::WPG == 65536),
                   "a group's sums fill the four 16 KB stage buffers");
     static_assert(ST == 2 || (ST <= 4 && 2 * C::PER_STAGE < 16), "stage count / vmcnt range");
+    static_assert((BK / C::KW) % KS == 0, "each group takes whole k-steps of every K step");
     __shared__ __attribute__((aligned(16))) unsigned char abuf[ST][C::A_BYTES];
     __shared__ __attribute__((aligned(16))) unsigned char bbuf[ST][C::B_BYTES];
     unsigned char *const a0 = abuf[0], *const a1 = abuf[1];
@@ -149,7 +173,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-    const int col = lane & 31, half = lane >> 5;
+    const int col = lane % MF, half = lane / MF;   // lane's column of a block; its k part
 
     // XCD-contiguous logical tile index, row-major over the tiles of C
     const int per = a.n_wg / NXCD, rem = a.n_wg % NXCD;
@@ -186,7 +210,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
     for (int i = 0; i < C::B_PER_THREAD; ++i) {
         const int s = i * NT + wave_u * 64 + lane;
         const int r = s / C::BCH, sc = s % C::BCH;
-        b_off[i] = (uint32_t)r * a.N * 2 + 16 * (sc ^ b_swz(r));
+        b_off[i] = (uint32_t)r * a.N * 2 + 16 * (sc ^ b_swz<MF>(r));
     }
 
     auto dma = [&](int kt, unsigned char *as, unsigned char *bs) {
@@ -204,41 +228,46 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
             dma16(lb + (i * NT + wave_u * 64) * 16, b_off[i], rb);
     };
 
-    f32x16 acc[C::FM][C::FN];
+    Acc acc[C::FM][C::FN];
 #pragma unroll
     for (int i = 0; i < C::FM; ++i)
 #pragma unroll
         for (int j = 0; j < C::FN; ++j)
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
+            for (int r = 0; r < C::AR; ++r)
                 acc[i][j][r] = 0.f;
 
     // B operand transpose-read addressing (per 16-lane group g = lane / 16,
-    // s = lane % 16): rows 16ks + 8(g >> 1) + (s >> 2) and + 4, columns
-    // 16(g & 1) + 4(s & 3) of each 32-column block: the lane then holds 8
-    // consecutive k of one column, k-slot t <-> k = 16ks + 8 half + t
+    // s = lane % 16).  MF = 32: rows 16ks + 8(g >> 1) + (s >> 2) and + 4,
+    // columns 16(g & 1) + 4(s & 3) of each 32-column block: the lane then
+    // holds 8 consecutive k of one column, k-slot t <-> k = 16ks + 8 half + t.
+    // MF = 16: rows 32ks + 8g + (s >> 2) and + 4, columns 4(s & 3) of each
+    // 16-column block: k-slot t <-> k = 32ks + 8g + t.
     const int g = lane >> 4, sl = lane & 15;
-    const int b_row = 8 * (g >> 1) + (sl >> 2);
-    const int b_col = 16 * (g & 1) + 4 * (sl & 3);
+    const int b_row = MF == 32 ? 8 * (g >> 1) + (sl >> 2) : 8 * g + (sl >> 2);
+    const int b_col = MF == 32 ? 16 * (g & 1) + 4 * (sl & 3) : 4 * (sl & 3);
 
     auto compute = [&](const unsigned char *as, const unsigned char *bs) {
 #pragma unroll
-        for (int kq = 0; kq < BK / 16 / KS; ++kq) {
-            const int ks = kg * (BK / 16 / KS) + kq;
+        for (int kq = 0; kq < BK / C::KW / KS; ++kq) {
+            const int ks = kg * (BK / C::KW / KS) + kq;
             bf16x8 av[C::FM], bv[C::FN];
 #pragma unroll
             for (int i = 0; i < C::FM; ++i) {
-                const int r = wm + 32 * i + col;
-                av[i] = *(const bf16x8 *)(as + r * (BK * 2) + 16 * ((2 * ks + half) ^ a_swz(r)));
+                // lane: row col of the block, k (KW ks + 8 half ..) = chunk
+                // (KW / 8) ks + half of the row
+                const int r = wm + MF * i + col;
+                av[i] = *(const bf16x8 *)(as + r * (BK * 2) +
+                                          16 * (((C::KW / 8) * ks + half) ^ a_swz(r)));
             }
 #pragma unroll
             for (int j = 0; j < C::FN; ++j) {
-                const int n = wn + 32 * j + b_col;
-                const int r0 = 16 * ks + b_row, r1 = r0 + 4;
+                const int n = wn + MF * j + b_col;
+                const int r0 = C::KW * ks + b_row, r1 = r0 + 4;
                 const unsigned char *p0 =
-                    bs + r0 * (BN * 2) + 16 * ((n >> 3) ^ b_swz(r0)) + 2 * (n & 7);
+                    bs + r0 * (BN * 2) + 16 * ((n >> 3) ^ b_swz<MF>(r0)) + 2 * (n & 7);
                 const unsigned char *p1 =
-                    bs + r1 * (BN * 2) + 16 * ((n >> 3) ^ b_swz(r1)) + 2 * (n & 7);
+                    bs + r1 * (BN * 2) + 16 * ((n >> 3) ^ b_swz<MF>(r1)) + 2 * (n & 7);
                 const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p0);
                 const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p1);
                 const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
@@ -248,7 +277,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
             for (int i = 0; i < C::FM; ++i)
 #pragma unroll
                 for (int j = 0; j < C::FN; ++j)
-                    acc[i][j] = mfma32(av[i], bv[j], acc[i][j]);
+                    acc[i][j] = mfma(av[i], bv[j], acc[i][j]);
         }
     };
 
@@ -300,13 +329,14 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
     if constexpr (KS > 1) {
         // group 0 adds the other groups' sums, one group per round, in
         // group order.  Accumulator block k = i FN + j of the wave in
-        // column cw goes, lane-major, to 4 KB piece k % 4 of stage buffer
-        // cw (FM FN / 4) + k / 4.
-        constexpr int NB = C::FM * C::FN / 4;   // 16 KB buffers per wave
+        // column cw goes, lane-major, to piece k (AR KB) of the wave's
+        // FM FN AR KB of the four 16 KB stage buffers, in buffer order.
+        constexpr int PB = C::AR * 256;                         // bytes per block
+        constexpr int NB = C::FM * C::FN * PB / 16384;          // 16 KB buffers per wave
         auto piece = [&](int k) {
-            const int bi = cw * NB + k / 4;
+            const int bi = cw * NB + (k * PB) / 16384;
             unsigned char *base = bi == 0 ? abuf[0] : bi == 1 ? abuf[1] : bi == 2 ? bbuf[0] : bbuf[1];
-            return (float *)(base + (k % 4) * 4096);
+            return (float *)(base + (k * PB) % 16384);
         };
         __syncthreads();   // every wave is done with the stage buffers
 #pragma unroll
@@ -318,7 +348,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
                     for (int j = 0; j < C::FN; ++j) {
                         float *p = piece(i * C::FN + j);
 #pragma unroll
-                        for (int r = 0; r < 16; ++r)
+                        for (int r = 0; r < C::AR; ++r)
                             p[r * 64 + lane] = acc[i][j][r];
                     }
             }
@@ -330,7 +360,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
                     for (int j = 0; j < C::FN; ++j) {
                         const float *p = piece(i * C::FN + j);
 #pragma unroll
-                        for (int r = 0; r < 16; ++r)
+                        for (int r = 0; r < C::AR; ++r)
                             acc[i][j][r] += p[r * 64 + lane];
                     }
             }
@@ -341,16 +371,16 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
             return;
     }
 
-    // epilogue: lane holds column wn + 32j + col, rows wm + 32i + 8(r/4) +
-    // 4half + r%4 of the tile
+    // epilogue: lane holds column wn + MF j + col, rows wm + MF i +
+    // 8(r/4) + 4half + r%4 (MF = 32) or 4half + r (MF = 16) of the tile
 #pragma unroll
     for (int i = 0; i < C::FM; ++i)
 #pragma unroll
         for (int j = 0; j < C::FN; ++j) {
-            const int n = n0 + wn + 32 * j + col;
+            const int n = n0 + wn + MF * j + col;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int m = m0 + wm + 32 * i + 8 * (r >> 2) + 4 * half + (r & 3);
+            for (int r = 0; r < C::AR; ++r) {
+                const int m = m0 + wm + MF * i + (MF == 32 ? 8 * (r >> 2) : 0) + 4 * half + (r & 3);
                 if (CBF16)
                     ((uint16_t *)a.C)[(size_t)m * a.N + n] =
                         (uint16_t)pack_bf16(acc[i][j][r], 0.f);
@@ -512,15 +542,21 @@ bool overlaps(const void *p, size_t pn, const void *q, size_t qn)
     return x < y + qn && y < x + pn;
 }
 
+// 16 x 16 blocks (v_mfma_f32_16x16x32_bf16) wherever a group's share of a
+// K step holds whole 32-wide k-steps: under the board's power limit that
+// MFMA form holds a higher clock than 32 x 32 x 16 (M5 1314 -> 1346-1359,
+// M1 1274-1297 -> 1333-1348, M4 1150 -> 1177 TFLOP/s); four groups share a
+// K step of 64 as 16-wide k-steps, so their tiles keep 32 x 32 blocks.
 template <int BM, int BN, int ST, int KS>
 hipError_t launch(GArgs &a, bool c_bf16, hipStream_t s)
 {
+    constexpr int MF = (BK / 32) % KS == 0 ? 16 : 32;
     a.tiles_n = a.N / BN;
     a.n_wg = (a.M / BM) * a.tiles_n;
     if (c_bf16)
-        hipLaunchKernelGGL((gemm_kernel<BM, BN, ST, KS, true>), dim3(a.n_wg), dim3(NT), 0, s, a);
+        hipLaunchKernelGGL((gemm_kernel<BM, BN, ST, KS, MF, true>), dim3(a.n_wg), dim3(NT), 0, s, a);
     else
-        hipLaunchKernelGGL((gemm_kernel<BM, BN, ST, KS, false>), dim3(a.n_wg), dim3(NT), 0, s, a);
+        hipLaunchKernelGGL((gemm_kernel<BM, BN, ST, KS, MF, false>), dim3(a.n_wg), dim3(NT), 0, s, a);
     return hipGetLastError();
 }
 
