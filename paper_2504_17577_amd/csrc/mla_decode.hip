@@ -25,7 +25,10 @@
 //    in the B-operand layout (the MFMA's 32-position reduction order is
 //    chosen to match), and V^T comes from the same latent rows in LDS through
 //    the transpose read ds_read_b64_tr_b16.  The P V of tile j-1 is issued
-//    after the score MFMAs of tile j, so it overlaps tile j's softmax.
+//    after the score MFMAs of tile j, and the 68 MFMAs of a tile run as one
+//    software pipeline whose LDS operands are read three MFMAs ahead (with
+//    every register given to the query and the accumulator, the compiler's
+//    own schedule read each operand just before its MFMA and waited for it).
 //  * Cache tiles of 32 positions go global -> LDS by DMA (buffer_load_dwordx4
 //    ... lds) into a ring of four buffers, two tiles ahead of the one in
 //    use: the latent part [32][512] and the rotary part [32][64] of a tile
@@ -62,6 +65,7 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 
 constexpr int DL = 512;              // latent width (query, cache, output)
 constexpr int DR = 64;               // rotary width (query, key)
@@ -77,6 +81,7 @@ constexpr int LAT_BYTES = BN * DL * 2;
 constexpr int ROT_BYTES = BN * DR * 2;
 constexpr int STAGE_BYTES = LAT_BYTES + ROT_BYTES;
 constexpr int NST = 4;               // ring buffers
+constexpr int PF = 3;                // MFMA operands read ahead of their MFMA
 constexpr int LAT_PER_THREAD = BN * (DL / 8) / NT;   // 16-byte latent DMA chunks per thread
 constexpr int ROT_THREADS = BN * (DR / 8);           // threads with one rotary chunk each
 constexpr int NXCD = 8;
@@ -157,8 +162,8 @@ struct Mla {
     bool rot_wave;                  // this wave also fetches rotary chunks
     const uint16_t *kv_b, *kpe_b;   // cache of (batch, latent head) at position 0
     uint32_t lat_off[2], rot_off;   // per-lane DMA source offsets (see init_lanes)
-    uint32_t ka[4], ra[2];          // per-lane LDS offsets of the score operands
-    uint32_t va[8];                 // ... of the value transpose reads
+    uint32_t ka0, ra0;              // per-lane LDS offsets of the score operands
+    uint32_t va0;                   // ... of the value transpose reads
     bf16x8 qreg[KS];                // the query of head hc: dims 32kk + 8gq .. +8
     f32x4 acc_o[DBO];
     float m_run, l_run;
@@ -190,16 +195,10 @@ struct Mla {
         }
         const int rr = 8 * (wave_u & 3) + lane / 8;
         rot_off = rr * rot_pitch + 16 * ((lane % 8) ^ rot_swz(rr));
-#pragma unroll
-        for (int m = 0; m < 4; ++m)
-            ka[m] = hc * (DL * 2) + 16 * ((4 * m + gq) ^ lat_swz(hc));
-#pragma unroll
-        for (int m = 0; m < 2; ++m)
-            ra[m] = LAT_BYTES + hc * (DR * 2) + 16 * ((4 * m + gq) ^ (hc >> 1));
+        ka0 = hc * (DL * 2) + 16 * (gq ^ lat_swz(hc));
+        ra0 = LAT_BYTES + hc * (DR * 2) + 16 * (gq ^ (hc >> 1));
         const int row = 4 * gq + (hc >> 2);
-#pragma unroll
-        for (int m = 0; m < 8; ++m)
-            va[m] = row * (DL * 2) + 16 * ((2 * m + ((hc & 3) >> 1)) ^ lat_swz(row)) + 8 * (hc & 1);
+        va0 = row * (DL * 2) + 16 * (((hc & 3) >> 1) ^ lat_swz(row)) + 8 * (hc & 1);
     }
 
     // DMA cache tile j (positions j*BN ..) into `stage`.  Each buffer
@@ -243,46 +242,75 @@ struct Mla {
         }
     }
 
-    // S^T[position][head] of the tile's two 16-position blocks, each as two
-    // interleaved accumulation chains over the 18 k-steps
-    __device__ __forceinline__ void scores(const unsigned char *stage, f32x4 (&s)[2]) const
+    // The tile's MFMA work as one software pipeline: the score MFMAs of the
+    // tile in `ss` (S^T[position][head] of its two 16-position blocks, 18
+    // k-steps each, SC) and then the P V of the previous tile, whose rows are
+    // in `sv` and whose weights are pk (PV).  Each MFMA's LDS operand is read
+    // PF MFMAs ahead, and scheduling barriers keep that order, so the LDS
+    // latency is covered by the MFMAs in between.
+    //   P V: O^T += V^T P^T over all 512 dims; the weights pk are in the
+    // B-operand layout (k-slot t of lane group gq is position 4gq + t for
+    // t < 4, 16 + 4gq + t - 4 after), V^T comes through the transpose reads.
+    template <bool SC, bool PV>
+    __device__ __forceinline__ void mma(const unsigned char *ss, const unsigned char *sv,
+                                        f32x4 (&s)[2], const uint32_t (&pk)[4])
     {
-        f32x4 c[2][2];
-#pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-            for (int h = 0; h < 2; ++h)
-                c[b][h] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kk = 0; kk < KS; ++kk)
-#pragma unroll
-            for (int b = 0; b < 2; ++b) {
-                const unsigned char *p =
-                    kk < KSL ? stage + ka[kk & 3] + 256 * (kk >> 2) + 16 * (DL * 2) * b
-                             : stage + ra[kk - KSL] + 16 * (DR * 2) * b;
-                const bf16x8 av = *(const bf16x8 *)p;
-                c[b][kk & 1] = mfma16(av, qreg[kk], c[b][kk & 1]);
-            }
-        s[0] = c[0][0] + c[0][1];
-        s[1] = c[1][0] + c[1][1];
-    }
-
-    // O^T += V^T P^T for one tile: the weights pk (B-operand layout: k-slot t
-    // of lane group gq is position 4gq + t for t < 4, 16 + 4gq + t - 4 after)
-    // and the transpose reads of the tile's latent rows, all 512 dims
-    __device__ __forceinline__ void pv(const uint32_t (&pk)[4], const unsigned char *stage)
-    {
+        constexpr int NS = SC ? 2 * KS : 0;
+        constexpr int N = NS + (PV ? DBO : 0);
         const bf16x8 bv = __builtin_bit_cast(bf16x8, u32x4{pk[0], pk[1], pk[2], pk[3]});
-#pragma unroll
-        for (int db = 0; db < DBO; ++db) {
-            const unsigned char *p = stage + va[db & 7] + 256 * (db >> 3);
-            const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p);
+        // The operand offsets of chunk index c ^ swizzle differ from those of
+        // c = 0 in the XOR of c's own bits (the swizzle and the row base
+        // occupy other bits), and the ring is aligned so that adding a stage
+        // base keeps that true: the latent score operand of k-step 4q + m is
+        // at (ka0 ^ 64m) + 256q, the rotary one of k-step 16 + m at ra0 ^ 64m,
+        // the value rows of block 8g + m at (va0 ^ 32m) + 256g.
+        const uint32_t kb = tileattn_dma::lds_addr(ss) + ka0;
+        const uint32_t rb = tileattn_dma::lds_addr(ss) + ra0;
+        const uint32_t vb = tileattn_dma::lds_addr(sv) + va0;
+        // Items i < NS are score MFMAs: k-step kk_of(i) of position block
+        // i & 1; items NS + v are P V MFMAs of output block db_of(v).  Both
+        // orders keep m, the XOR term, fixed for four items in a row.
+        auto kk_of = [](int i) {
+            const int u = i >> 1;   // 0 .. 17
+            return u < KSL ? 4 * (u & 3) + (u >> 2) : u;
+        };
+        auto db_of = [](int v) { return 8 * (v & 3) + (v >> 2); };
+        auto operand = [&](int i) -> bf16x8 {
+            if (i < NS) {
+                const int kk = kk_of(i), b = i & 1;
+                const uint32_t p = kk < KSL
+                    ? (kb ^ (64u * (kk & 3))) + 256u * (kk >> 2) + 16u * (DL * 2) * b
+                    : (rb ^ (64u * (kk - KSL))) + 16u * (DR * 2) * b;
+                return *(const lds_bf16x8 *)(uintptr_t)p;
+            }
+            const int db = db_of(i - NS);
+            const uint32_t p = (vb ^ (32u * (db & 7))) + 256u * (db >> 3);
+            const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(uintptr_t)p);
             const i16x4 hi =
-                __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(p + 16 * (DL * 2)));
+                __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(uintptr_t)(p + 16u * (DL * 2)));
             const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
-            const u32x4 aw = {l2[0], l2[1], h2[0], h2[1]};
-            acc_o[db] = mfma16(__builtin_bit_cast(bf16x8, aw), bv, acc_o[db]);
+            return __builtin_bit_cast(bf16x8, u32x4{l2[0], l2[1], h2[0], h2[1]});
+        };
+        if (SC) {
+            s[0] = f32x4{0.f, 0.f, 0.f, 0.f};
+            s[1] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
+        bf16x8 buf[PF];
+#pragma unroll
+        for (int i = 0; i < PF; ++i)
+            if (i < N)
+                buf[i] = operand(i);
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            __builtin_amdgcn_sched_barrier(0);
+            if (i < NS)
+                s[i & 1] = mfma16(buf[i % PF], qreg[kk_of(i)], s[i & 1]);
+            else
+                acc_o[db_of(i - NS)] = mfma16(buf[i % PF], bv, acc_o[db_of(i - NS)]);
+            if (i + PF < N)
+                buf[i % PF] = operand(i + PF);
+        }
+        __builtin_amdgcn_sched_barrier(0);
     }
 
     // Online softmax of tile j: mask, running max, weights into pk
@@ -339,7 +367,7 @@ struct Mla {
     // t+2 goes into the stage of tile t-2; then the scores of tile t, the
     // P V of tile t-1 (weights pk, rows in stage (t-1) % 4) and the softmax
     // of tile t, whose weights replace pk.
-    template <bool MASKED>
+    template <bool MASKED, bool FIRST>
     __device__ __forceinline__ void step(int t, int n, int j_lo, unsigned char *ring,
                                          uint32_t (&pk)[4])
     {
@@ -351,9 +379,8 @@ struct Mla {
         if (t + 2 < n)
             dma_tile(j_lo + t + 2, ring + ((t + 2) % NST) * STAGE_BYTES);
         f32x4 s[2];
-        scores(ring + (t % NST) * STAGE_BYTES, s);
-        if (t > 0)
-            pv(pk, ring + ((t + NST - 1) % NST) * STAGE_BYTES);
+        mma<true, !FIRST>(ring + (t % NST) * STAGE_BYTES, ring + ((t + NST - 1) % NST) * STAGE_BYTES,
+                          s, pk);
         softmax<MASKED>(j_lo + t, s, pk);
     }
 };
@@ -377,7 +404,7 @@ __device__ __forceinline__ void decode_wg(const MArgs &a, int bid, int &b, int &
 
 __global__ __launch_bounds__(NT, 1) void mla_decode_kernel(MArgs args)
 {
-    __shared__ __attribute__((aligned(16))) unsigned char ring[NST * STAGE_BYTES];
+    __shared__ __attribute__((aligned(1024))) unsigned char ring[NST * STAGE_BYTES];
 
     Mla k(args);
     const MArgs &a = args;
@@ -437,13 +464,20 @@ __global__ __launch_bounds__(NT, 1) void mla_decode_kernel(MArgs args)
     // every tile but a ragged last one is fully valid
     const int n_full = min(j_hi, a.Skv / BN) - j_lo;
     uint32_t pk[4];
-    int t = 0;
+    if (n_full > 0)
+        k.step<false, true>(0, n, j_lo, ring, pk);
+    else
+        k.step<true, true>(0, n, j_lo, ring, pk);
+    int t = 1;
     for (; t < n_full; ++t)
-        k.step<false>(t, n, j_lo, ring, pk);
+        k.step<false, false>(t, n, j_lo, ring, pk);
     if (t < n)
-        k.step<true>(t, n, j_lo, ring, pk);
+        k.step<true, false>(t, n, j_lo, ring, pk);
     // the last tile's P V
-    k.pv(pk, ring + ((n - 1) % NST) * STAGE_BYTES);
+    {
+        f32x4 s_unused[2];
+        k.mma<false, true>(ring, ring + ((n - 1) % NST) * STAGE_BYTES, s_unused, pk);
+    }
 
     // epilogue: normalise and store the split's result of the lane's head:
     // block db, lane group gq holds dims 16db + 4gq .. +3
