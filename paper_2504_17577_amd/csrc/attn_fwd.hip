@@ -83,6 +83,8 @@ constexpr int BM_SMALL = 64; // the same with 16 query rows per wave (small grid
 constexpr int BN = 64;       // keys per tile
 constexpr int NT = 256;      // threads per workgroup
 constexpr int NXCD = 8;      // XCDs per MI355X
+constexpr int PF_S = 4;      // score MFMA operands read ahead of their MFMA
+constexpr int PF_V = 3;      // P V MFMA operands read ahead of their MFMA
 constexpr float LOG2E = 1.44269504088896340736f;
 constexpr float LN2 = 0.69314718055994530942f;
 constexpr float RESCALE_SLACK = 8.0f;   // base-2 headroom: weights never exceed 2^8
@@ -379,7 +381,10 @@ struct Kernel {
         dma_tile<true>(a.V + kv_base, j, stage + C::TILE_BYTES);
     }
 
-    // S^T[key][query] of one tile (NKB blocks of QW keys, chains interleaved)
+    // S^T[key][query] of one tile (NKB blocks of QW keys, chains interleaved).
+    // Each MFMA's K operand is read PF_S MFMAs ahead and scheduling barriers
+    // keep that order (the compiler's own schedule kept one to three reads
+    // in flight); the P V product below does the same with PF_V.
     __device__ __forceinline__ void scores(const unsigned char *kbuf, Acc (&s)[NKB]) const
     {
 #pragma unroll
@@ -387,15 +392,26 @@ struct Kernel {
 #pragma unroll
             for (int r = 0; r < AR; ++r)
                 s[b][r] = 0.f;
+        constexpr int N = KK * NKB;
+        auto operand = [&](int i) -> bf16x8 {
+            const int kk = i / NKB, b = i % NKB;
+            const int row = QW * b + col;
+            const int ch = (NG * kk + half) ^ C::kswz(row);
+            return *(const bf16x8 *)(kbuf + row * (D * 2) + ch * 16);
+        };
+        bf16x8 buf[PF_S];
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk)
+        for (int i = 0; i < PF_S; ++i)
+            if (i < N)
+                buf[i] = operand(i);
 #pragma unroll
-            for (int b = 0; b < NKB; ++b) {
-                const int row = QW * b + col;
-                const int ch = (NG * kk + half) ^ C::kswz(row);
-                const bf16x8 av = *(const bf16x8 *)(kbuf + row * (D * 2) + ch * 16);
-                s[b] = mfma(av, qreg[kk], s[b]);
-            }
+        for (int i = 0; i < N; ++i) {
+            __builtin_amdgcn_sched_barrier(0);
+            s[i % NKB] = mfma(buf[i % PF_S], qreg[i / NKB], s[i % NKB]);
+            if (i + PF_S < N)
+                buf[i % PF_S] = operand(i + PF_S);
+        }
+        __builtin_amdgcn_sched_barrier(0);
     }
 
     // key (within the tile) of accumulator value r of block b
@@ -484,35 +500,54 @@ struct Kernel {
             // MFMA k-slot t of half h stands for key 16ks + 4h + t (t < 4) or
             // 16ks + 8 + 4h + t-4, matching where the accumulator layout left P
             const int gq = lane >> 4;
+            constexpr int N = (BN / 16) * DB;
+            auto operand = [&](int i) -> bf16x8 {
+                const int ks = i / DB, db = i % DB;
+                const int row0 = 16 * ks + 4 * half + (sl >> 2);
+                const int d = 32 * db + 16 * (gq & 1) + 4 * (sl & 3);
+                return v_operand(vbuf, row0, row0 + 8, d);
+            };
+            bf16x8 buf[PF_V];
 #pragma unroll
-            for (int ks = 0; ks < BN / 16; ++ks) {
+            for (int i = 0; i < PF_V; ++i)
+                if (i < N)
+                    buf[i] = operand(i);
+#pragma unroll
+            for (int i = 0; i < N; ++i) {
+                __builtin_amdgcn_sched_barrier(0);
+                const int ks = i / DB, db = i % DB;
                 const int b = ks >> 1, rb = (ks & 1) * 4;
                 const u32x4 bw = {pk[b][rb], pk[b][rb + 1], pk[b][rb + 2], pk[b][rb + 3]};
-                const bf16x8 bv = __builtin_bit_cast(bf16x8, bw);
-                const int row0 = 16 * ks + 4 * half + (sl >> 2);
-                const int row1 = row0 + 8;
-#pragma unroll
-                for (int db = 0; db < DB; ++db) {
-                    const int d = 32 * db + 16 * (gq & 1) + 4 * (sl & 3);
-                    acc_o[db] = mfma(v_operand(vbuf, row0, row1, d), bv, acc_o[db]);
-                }
+                acc_o[db] = mfma(buf[i % PF_V], __builtin_bit_cast(bf16x8, bw), acc_o[db]);
+                if (i + PF_V < N)
+                    buf[i % PF_V] = operand(i + PF_V);
             }
+            __builtin_amdgcn_sched_barrier(0);
         } else {
             // MFMA k-slot t of quarter g stands for key 32ks + 4g + t (t < 4)
             // or 32ks + 16 + 4g + t-4: blocks 2ks and 2ks+1 of the scores
+            constexpr int N = (BN / 32) * DB;
+            auto operand = [&](int i) -> bf16x8 {
+                const int ks = i / DB, db = i % DB;
+                const int row0 = 32 * ks + 4 * half + (sl >> 2);
+                return v_operand(vbuf, row0, row0 + 16, 16 * db + 4 * (sl & 3));
+            };
+            bf16x8 buf[PF_V];
 #pragma unroll
-            for (int ks = 0; ks < BN / 32; ++ks) {
+            for (int i = 0; i < PF_V; ++i)
+                if (i < N)
+                    buf[i] = operand(i);
+#pragma unroll
+            for (int i = 0; i < N; ++i) {
+                __builtin_amdgcn_sched_barrier(0);
+                const int ks = i / DB, db = i % DB;
                 const u32x4 bw = {pk[2 * ks][0], pk[2 * ks][1], pk[2 * ks + 1][0],
                                   pk[2 * ks + 1][1]};
-                const bf16x8 bv = __builtin_bit_cast(bf16x8, bw);
-                const int row0 = 32 * ks + 4 * half + (sl >> 2);
-                const int row1 = row0 + 16;
-#pragma unroll
-                for (int db = 0; db < DB; ++db) {
-                    const int d = 16 * db + 4 * (sl & 3);
-                    acc_o[db] = mfma(v_operand(vbuf, row0, row1, d), bv, acc_o[db]);
-                }
+                acc_o[db] = mfma(buf[i % PF_V], __builtin_bit_cast(bf16x8, bw), acc_o[db]);
+                if (i + PF_V < N)
+                    buf[i % PF_V] = operand(i + PF_V);
             }
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 
