@@ -60,7 +60,8 @@ def test_gemm_full_compare(ta, shape):
     check(f"gemm {shape}", c, a, b)
 
 
-@pytest.mark.parametrize("name", ["gemm_m0", "gemm_m4", "gemm_m5", "gemm_m3", "gemm_m1"])
+@pytest.mark.parametrize("name", ["gemm_m0", "gemm_m4", "gemm_m5", "gemm_m3", "gemm_m1",
+                                  "gemm_m2", "gemm_m6", "gemm_m7"])
 def test_gemm_workload_sampled(ta, name):
     """The paper's shapes at full size (all three tile configurations):
     sampled rows against the oracle, every element finite."""
@@ -117,7 +118,7 @@ def test_gemv_full_compare(ta, shape):
 
 
 @pytest.mark.parametrize("name", ["gemv_v5", "gemv_v7", "gemv_v0", "gemv_v6", "gemv_v1",
-                                  "gemv_v4"])
+                                  "gemv_v4", "gemv_v2", "gemv_v3"])
 def test_gemv_workload_sampled(ta, name):
     """The paper's matrix-vector shapes at full size: every output finite,
     sampled columns (first and last of strips, random ones) against the
