@@ -25,8 +25,9 @@
 //    in the B-operand layout (the MFMA's 32-position reduction order is
 //    chosen to match), and V^T comes from the same latent rows in LDS through
 //    the transpose read ds_read_b64_tr_b16.  The P V of tile j-1 is issued
-//    after the score MFMAs of tile j, and the 68 MFMAs of a tile run as one
-//    software pipeline whose LDS operands are read three MFMAs ahead (with
+//    among the score MFMAs of tile j (alternately), and the 68 MFMAs of a
+//    tile run as one software pipeline whose LDS operands are read three
+//    MFMAs ahead (with
 //    every register given to the query and the accumulator, the compiler's
 //    own schedule read each operand just before its MFMA and waited for it).
 //  * Cache tiles of 32 positions go global -> LDS by DMA (buffer_load_dwordx4
@@ -244,10 +245,13 @@ struct Mla {
 
     // The tile's MFMA work as one software pipeline: the score MFMAs of the
     // tile in `ss` (S^T[position][head] of its two 16-position blocks, 18
-    // k-steps each, SC) and then the P V of the previous tile, whose rows are
-    // in `sv` and whose weights are pk (PV).  Each MFMA's LDS operand is read
-    // PF MFMAs ahead, and scheduling barriers keep that order, so the LDS
-    // latency is covered by the MFMAs in between.
+    // k-steps each, SC) and the P V of the previous tile, whose rows are in
+    // `sv` and whose weights are pk (PV), issued alternately while both
+    // remain (a score MFMA's operand is one ds_read_b128, a P V MFMA's two
+    // transpose reads: mixed, the two kinds of read keep the LDS busier than
+    // in two separate phases).  Each MFMA's LDS operand is read PF MFMAs
+    // ahead, and scheduling barriers keep that order, so the LDS latency is
+    // covered by the MFMAs in between.
     //   P V: O^T += V^T P^T over all 512 dims; the weights pk are in the
     // B-operand layout (k-slot t of lane group gq is position 4gq + t for
     // t < 4, 16 + 4gq + t - 4 after), V^T comes through the transpose reads.
@@ -295,20 +299,31 @@ struct Mla {
             s[0] = f32x4{0.f, 0.f, 0.f, 0.f};
             s[1] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
+        // issue order: score and P V items alternate while both remain
+        constexpr int NPV = N - NS;
+        auto item = [](int x) {
+            if (NS == 0 || NPV == 0)
+                return x;
+            const int m2 = NPV < NS ? NPV : NS;
+            if (x < 2 * m2)
+                return (x & 1) ? NS + (x >> 1) : (x >> 1);
+            return NS > NPV ? x - m2 : NS + (x - m2);
+        };
         bf16x8 buf[PF];
 #pragma unroll
         for (int i = 0; i < PF; ++i)
             if (i < N)
-                buf[i] = operand(i);
+                buf[i] = operand(item(i));
 #pragma unroll
-        for (int i = 0; i < N; ++i) {
+        for (int x = 0; x < N; ++x) {
             __builtin_amdgcn_sched_barrier(0);
+            const int i = item(x);
             if (i < NS)
-                s[i & 1] = mfma16(buf[i % PF], qreg[kk_of(i)], s[i & 1]);
+                s[i & 1] = mfma16(buf[x % PF], qreg[kk_of(i)], s[i & 1]);
             else
-                acc_o[db_of(i - NS)] = mfma16(buf[i % PF], bv, acc_o[db_of(i - NS)]);
-            if (i + PF < N)
-                buf[i % PF] = operand(i + PF);
+                acc_o[db_of(i - NS)] = mfma16(buf[x % PF], bv, acc_o[db_of(i - NS)]);
+            if (x + PF < N)
+                buf[x % PF] = operand(item(x + PF));
         }
         __builtin_amdgcn_sched_barrier(0);
     }
