@@ -161,6 +161,8 @@ struct Mla {
     int wave, lane, hc, gq;         // hc = lane % 16 (the head), gq = lane / 16
     int wave_u;                     // the wave index, in a scalar register
     bool rot_wave;                  // this wave also fetches rotary chunks
+    bool busy;                      // some of this wave's 16 heads exist (else it only
+                                    // takes part in the tile DMA and the barriers)
     const uint16_t *kv_b, *kpe_b;   // cache of (batch, latent head) at position 0
     uint32_t lat_off[2], rot_off;   // per-lane DMA source offsets (see init_lanes)
     uint32_t ka0, ra0;              // per-lane LDS offsets of the score operands
@@ -393,10 +395,12 @@ struct Mla {
         __syncthreads();
         if (t + 2 < n)
             dma_tile(j_lo + t + 2, ring + ((t + 2) % NST) * STAGE_BYTES);
-        f32x4 s[2];
-        mma<true, !FIRST>(ring + (t % NST) * STAGE_BYTES, ring + ((t + NST - 1) % NST) * STAGE_BYTES,
-                          s, pk);
-        softmax<MASKED>(j_lo + t, s, pk);
+        if (busy) {
+            f32x4 s[2];
+            mma<true, !FIRST>(ring + (t % NST) * STAGE_BYTES,
+                              ring + ((t + NST - 1) % NST) * STAGE_BYTES, s, pk);
+            softmax<MASKED>(j_lo + t, s, pk);
+        }
     }
 };
 
@@ -442,6 +446,7 @@ __global__ __launch_bounds__(NT, 1) void mla_decode_kernel(MArgs args)
     const int h_loc = hblk * HB + k.wave_u * HW + k.hc;
     const bool head_ok = h_loc < a.g;
     const int head = hk * a.g + min(h_loc, a.g - 1);
+    k.busy = hblk * HB + k.wave_u * HW < a.g;   // wave-uniform
 
     k.kv_b = a.KV + ((size_t)b * a.Skv * a.Hkv + hk) * DL;
     k.kpe_b = a.Kpe + ((size_t)b * a.Skv * a.Hkv + hk) * DR;
@@ -491,7 +496,8 @@ __global__ __launch_bounds__(NT, 1) void mla_decode_kernel(MArgs args)
     // the last tile's P V
     {
         f32x4 s_unused[2];
-        k.mma<false, true>(ring, ring + ((n - 1) % NST) * STAGE_BYTES, s_unused, pk);
+        if (k.busy)
+            k.mma<false, true>(ring, ring + ((n - 1) % NST) * STAGE_BYTES, s_unused, pk);
     }
 
     // epilogue: normalise and store the split's result of the lane's head:
