@@ -22,9 +22,10 @@ oracle.
   python bench.py --workload gemm_m5 [--out f32|bf16]
                                     # C = A B (gemm_bf16) at one of the paper's
                                     # M0-M7 shapes, with hipBLASLt timed beside it
-  python bench.py --workload gemv_v0 [--out f32|bf16]
+  python bench.py --workload gemv_v0 [--out f32|bf16] [--splits 1|N|auto]
                                     # the same call at M = 1 (the paper's V0-V7
-                                    # matrix-vector shapes), HBM-bound
+                                    # matrix-vector shapes), HBM-bound; with more
+                                    # than one split, gemv_bf16_split
   python bench.py --workload mla_b64_s8k [--splits auto|N]
                                     # one multi-head latent attention decode step
                                     # (mla_decode) instead of attn_fwd
@@ -356,8 +357,24 @@ def bench_gemm(args, torch, tileattn):
     c = torch.empty((w.M, w.N), dtype=dt, device="cuda")
     stream = torch.cuda.current_stream()
 
+    gemv = w.M == 1
+    n_split = 1
+    if gemv:
+        # gemv_bf16_split (K split over workgroups, fp32 partials merged by a
+        # second kernel); 1 is gemm_bf16's matrix-vector kernel
+        n_split = (tileattn.gemv_split_heuristic(w.N, w.K) if args.splits == "auto"
+                   else int(args.splits))
+    elif args.splits != "1":
+        raise SystemExit("bench: --splits applies to attention, MLA and matrix-vector workloads")
+    ws = torch.empty(max(16, tileattn.gemv_split_workspace_bytes(w.N, n_split) if gemv else 16),
+                     dtype=torch.uint8, device="cuda")
+
     def step():
-        tileattn.gemm_bf16(da, db, out=c, out_dtype=dt, stream=stream)
+        if n_split > 1:
+            tileattn.gemv_bf16_split(da, db, num_splits=n_split, out=c, out_dtype=dt, workspace=ws,
+                                     stream=stream)
+        else:
+            tileattn.gemm_bf16(da, db, out=c, out_dtype=dt, stream=stream)
 
     def timed(fn):
         for _ in range(args.warmup):
@@ -374,7 +391,6 @@ def bench_gemm(args, torch, tileattn):
         return start.elapsed_time(end) / args.steps, time.perf_counter() - t0
 
     ms, wall = timed(step)
-    gemv = w.M == 1
     ref_out = torch.empty((w.M, w.N), dtype=torch.bfloat16, device="cuda")
     ms_ref, _ = timed(lambda: torch.matmul(da, db, out=ref_out))
     tflops = w.flops() / (ms * 1e-3) / 1e12
@@ -384,7 +400,7 @@ def bench_gemm(args, torch, tileattn):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "out_dtype": "bf16" if c_bf16 else "f32", "data": "synthetic",
         "config": {"workload": w.name, "shape": w.describe(), "M": w.M, "N": w.N, "K": w.K,
-                   "seed": args.seed, "flops_per_step": w.flops(),
+                   "splits": n_split, "seed": args.seed, "flops_per_step": w.flops(),
                    "bytes_per_step": w.bytes(2 if c_bf16 else 4)},
     }
     if gemv:
@@ -632,7 +648,8 @@ def main():
     ap.add_argument("--splits", default="1",
                     help="key splits per query tile: 1 (attn_fwd), N or auto "
                          "(attn_fwd_split with ta_split_heuristic; workspace allocated "
-                         "before the timed region)")
+                         "before the timed region); MLA: cache splits; matrix-vector "
+                         "workloads: K splits (gemv_bf16_split, gemv_split_heuristic)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--oracle-all-configs", action="store_true",
                     help="time the fp64 oracle on every element of the five target "

@@ -225,6 +225,44 @@ ta_status gemm_bf16(const void *A, const void *B, void *C, int c_bf16, int M, in
                     void *stream);
 
 /*
+ * gemv_bf16_split — the matrix-vector product C[n] = sum_k A[k] B[k][n] of
+ * gemm_bf16 with M == 1 (the paper's V0-V7 shapes, appendix table "Matrix
+ * shapes in our benchmark"), with the K rows split into num_splits ranges
+ * that separate workgroups sum, so that shapes with few column strips
+ * still occupy every CU.
+ *
+ *   A  device, bf16 [K]                       read only
+ *   B  device, bf16 [K, N] row-major          read only
+ *   C  device, [N]: fp32, or bf16 (rounded to nearest even once, from the
+ *      fp32 sum) if c_bf16 != 0                written
+ *   N % 64 == 0 and K % 8 == 0 (else TA_ERR_UNSUPPORTED)
+ *   num_splits: 1..64 (else TA_ERR_INVALID_SHAPE); 1 runs gemm_bf16's
+ *   matrix-vector kernel and ignores the workspace; for more, each range's
+ *   fp32 partial sums go to `workspace` (device, 16-byte aligned, at least
+ *   gemv_split_workspace_bytes(N, num_splits) bytes, owned by the caller, no
+ *   overlap with A, B or C; TA_ERR_WORKSPACE if NULL or smaller) and a
+ *   second kernel adds them in range order
+ *   every pointer 16-byte aligned; C must not overlap A or B; stream as
+ *   attn_fwd
+ * Status codes as attn_fwd; validation before any HIP call.  The result
+ * does not depend on timing; it differs from the unsplit kernel's in the
+ * grouping of the fp32 additions only.
+ */
+ta_status gemv_bf16_split(const void *A, const void *B, void *C, int c_bf16, int N, int K,
+                          int num_splits, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Workspace bytes gemv_bf16_split needs: num_splits * N * 4 for
+ * num_splits > 1, 0 for 1.  No HIP call. */
+ta_status gemv_split_workspace_bytes(int N, int num_splits, size_t *bytes);
+
+/* A split count for gemv_bf16_split.  A workgroup sums one strip of 256
+ * columns (N % 256 == 0, else 64) over one K range, and two fit a CU; the
+ * count chosen is the one whose workgroups (strips x splits, at most 512)
+ * fill their last round of the 256 CUs most evenly, with at least 1024 rows
+ * per range (fewer workgroups on a tie).  No HIP call. */
+ta_status gemv_split_heuristic(int N, int K, int *num_splits);
+
+/*
  * Mamba-2 state-space-duality (SSD) chunk functions: the paper's linear
  * attention workload ("chunk-scan and chunk-state functions from Mamba-2",
  * Section "Numerical Experiments", paragraph "Linear Attention Performance";

@@ -396,11 +396,14 @@ __global__ __launch_bounds__(NT, 2) void gemm_kernel(GArgs args)
 // workgroup of 16 waves owns a strip of COLS columns (COLS * 2 contiguous
 // bytes of each B row); a lane reads 16 bytes (8 columns) of a row, so one
 // load instruction covers RPL = 512 / COLS full row segments.  Rows are taken
-// in groups of 8, split evenly over the waves; a wave walks its groups RPL
+// in groups of 8 (SPLIT: the groups of key range blockIdx.y of gridDim.y),
+// split evenly over the waves; a wave walks its groups RPL
 // (or 2 RPL) at a time, lane g (of RPL) taking all 8 rows of group gi + g
 // (or 16 rows of groups gi + 2g, gi + 2g + 1), so that its values of a are
 // 16-byte loads.  Partial sums meet in LDS and COLS
-// threads add them in a fixed order (results do not depend on timing).
+// threads add them in a fixed order (results do not depend on timing); with
+// SPLIT the strip's sum over its range goes, in fp32, to row blockIdx.y of
+// the workspace C [gridDim.y][N] for gemv_combine_kernel.
 constexpr int GV_WAVES = 16;
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
@@ -418,7 +421,7 @@ __device__ __forceinline__ u32x4 ld_b(const uint16_t *p)
 }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-template <int COLS, bool NT, bool CBF16>
+template <int COLS, bool NT, bool CBF16, bool SPLIT>
 __global__ __launch_bounds__(64 * GV_WAVES) void gemv_kernel(const uint16_t *A, const uint16_t *B,
                                                               void *C, int N, int K)
 {
@@ -431,9 +434,14 @@ __global__ __launch_bounds__(64 * GV_WAVES) void gemv_kernel(const uint16_t *A, 
     const int n0 = blockIdx.x * COLS;
     const int g = lane / LPR;
     const int c8 = (lane % LPR) * 8;    // this lane's first column in the strip
-    const int groups = K / 8;
-    const int g0 = (int)((int64_t)groups * wave / GV_WAVES);
-    const int g1 = (int)((int64_t)groups * (wave + 1) / GV_WAVES);
+    int gb = 0, groups = K / 8;
+    if (SPLIT) {
+        const int all = groups, sp = blockIdx.y, ns = gridDim.y;
+        gb = (int)((int64_t)all * sp / ns);
+        groups = (int)((int64_t)all * (sp + 1) / ns) - gb;
+    }
+    const int g0 = gb + (int)((int64_t)groups * wave / GV_WAVES);
+    const int g1 = gb + (int)((int64_t)groups * (wave + 1) / GV_WAVES);
 
     float acc[8];
 #pragma unroll
@@ -500,11 +508,44 @@ __global__ __launch_bounds__(64 * GV_WAVES) void gemv_kernel(const uint16_t *A, 
 #pragma unroll
             for (int r = 0; r < RPL; ++r)
                 sum += red[w][r][tid];
-        if (CBF16)
+        if (SPLIT)
+            ((float *)C)[(size_t)blockIdx.y * N + n0 + tid] = sum;
+        else if (CBF16)
             ((uint16_t *)C)[n0 + tid] = (uint16_t)pack_bf16(sum, 0.f);
         else
             ((float *)C)[n0 + tid] = sum;
     }
+}
+
+// The merge of gemv_bf16_split: C[n] = W[0][n] + W[1][n] + ... + W[S-1][n],
+// added in that order (fp32), then rounded once if C is bf16.
+constexpr int GV_COMBINE = 256;
+template <bool CBF16>
+__global__ __launch_bounds__(GV_COMBINE) void gemv_combine_kernel(const float *W, void *C, int N,
+                                                                  int S)
+{
+    const int n = blockIdx.x * GV_COMBINE + threadIdx.x;
+    if (n >= N)
+        return;
+    const float *w = W + n;
+    float sum = w[0];
+    int s = 1;
+    // eight rows' loads in flight before their adds
+    for (; s + 8 <= S; s += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            v[u] = w[(size_t)(s + u) * N];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            sum += v[u];
+    }
+    for (; s < S; ++s)
+        sum += w[(size_t)s * N];
+    if (CBF16)
+        ((uint16_t *)C)[n] = (uint16_t)pack_bf16(sum, 0.f);
+    else
+        ((float *)C)[n] = sum;
 }
 
 // Strips of 256 columns (512-byte row segments) stream B faster than
@@ -515,24 +556,53 @@ template <bool NT, bool CBF16>
 hipError_t launch_gemv(const uint16_t *a, const uint16_t *b, void *C, int N, int K, hipStream_t s)
 {
     if (N % 256 == 0 && N / 256 >= 144)
-        hipLaunchKernelGGL((gemv_kernel<256, NT, CBF16>), dim3(N / 256), dim3(64 * GV_WAVES), 0, s,
-                           a, b, C, N, K);
+        hipLaunchKernelGGL((gemv_kernel<256, NT, CBF16, false>), dim3(N / 256), dim3(64 * GV_WAVES),
+                           0, s, a, b, C, N, K);
     else
-        hipLaunchKernelGGL((gemv_kernel<64, NT, CBF16>), dim3(N / 64), dim3(64 * GV_WAVES), 0, s,
-                           a, b, C, N, K);
+        hipLaunchKernelGGL((gemv_kernel<64, NT, CBF16, false>), dim3(N / 64), dim3(64 * GV_WAVES),
+                           0, s, a, b, C, N, K);
     return hipGetLastError();
 }
+
+// K split into S ranges: 256-column strips wherever N allows (their rows
+// stream faster), S workgroups per strip writing fp32 partial sums to W
+// [S][N], then the merge.
+template <bool NT>
+hipError_t launch_gemv_split(const uint16_t *a, const uint16_t *b, void *C, bool c_bf16, int N,
+                             int K, int S, float *W, hipStream_t s)
+{
+    if (N % 256 == 0)
+        hipLaunchKernelGGL((gemv_kernel<256, NT, false, true>), dim3(N / 256, S),
+                           dim3(64 * GV_WAVES), 0, s, a, b, (void *)W, N, K);
+    else
+        hipLaunchKernelGGL((gemv_kernel<64, NT, false, true>), dim3(N / 64, S), dim3(64 * GV_WAVES),
+                           0, s, a, b, (void *)W, N, K);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    const dim3 grid((N + GV_COMBINE - 1) / GV_COMBINE);
+    if (c_bf16)
+        hipLaunchKernelGGL(gemv_combine_kernel<true>, grid, dim3(GV_COMBINE), 0, s, W, C, N, S);
+    else
+        hipLaunchKernelGGL(gemv_combine_kernel<false>, grid, dim3(GV_COMBINE), 0, s, W, C, N, S);
+    return hipGetLastError();
+}
+
+// B larger than the 256 MB Infinity Cache: non-temporal loads
+bool gemv_nt(int N, int K) { return (size_t)K * N * 2 > ((size_t)256 << 20); }
 
 hipError_t run_gemv(const void *A, const void *B, void *C, bool c_bf16, int N, int K, hipStream_t s)
 {
     const auto a = (const uint16_t *)A, b = (const uint16_t *)B;
-    const bool nt = (size_t)K * N * 2 > ((size_t)256 << 20);
-    if (nt)
+    if (gemv_nt(N, K))
         return c_bf16 ? launch_gemv<true, true>(a, b, C, N, K, s)
                       : launch_gemv<true, false>(a, b, C, N, K, s);
     return c_bf16 ? launch_gemv<false, true>(a, b, C, N, K, s)
                   : launch_gemv<false, false>(a, b, C, N, K, s);
 }
+
+
+constexpr int GV_MAX_SPLITS = 64;
 
 bool misaligned(const void *p) { return ((uintptr_t)p & 15u) != 0; }
 
@@ -608,6 +678,85 @@ ta_status gemm_bf16(const void *A, const void *B, void *C, int c_bf16, int M, in
                          : ring ? launch<128, 128, 4, 4>(a, c_bf16 != 0, s)
                                 : launch<128, 128, 2, 2>(a, c_bf16 != 0, s);
     return e == hipSuccess ? TA_OK : TA_ERR_LAUNCH;
+}
+
+ta_status gemv_bf16_split(const void *A, const void *B, void *C, int c_bf16, int N, int K,
+                          int num_splits, void *workspace, size_t workspace_bytes, void *stream)
+{
+    if (!A || !B || !C)
+        return TA_ERR_NULL_POINTER;
+    if (N < 1 || K < 1 || num_splits < 1 || num_splits > GV_MAX_SPLITS)
+        return TA_ERR_INVALID_SHAPE;
+    if (N % 64 || K % 8)
+        return TA_ERR_UNSUPPORTED;
+    if (misaligned(A) || misaligned(B) || misaligned(C))
+        return TA_ERR_MISALIGNED;
+    const size_t a_bytes = (size_t)K * 2, b_bytes = (size_t)K * N * 2;
+    const size_t c_bytes = (size_t)N * (c_bf16 ? 2 : 4);
+    if (overlaps(C, c_bytes, A, a_bytes) || overlaps(C, c_bytes, B, b_bytes))
+        return TA_ERR_ALIASING;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    if (num_splits == 1) {
+        e = run_gemv(A, B, C, c_bf16 != 0, N, K, s);
+    } else {
+        const size_t w_bytes = (size_t)num_splits * N * 4;
+        if (!workspace || workspace_bytes < w_bytes)
+            return TA_ERR_WORKSPACE;
+        if (misaligned(workspace))
+            return TA_ERR_MISALIGNED;
+        if (overlaps(workspace, w_bytes, A, a_bytes) || overlaps(workspace, w_bytes, B, b_bytes) ||
+            overlaps(workspace, w_bytes, C, c_bytes))
+            return TA_ERR_ALIASING;
+        const auto a = (const uint16_t *)A, b = (const uint16_t *)B;
+        const auto w = (float *)workspace;
+        e = gemv_nt(N, K) ? launch_gemv_split<true>(a, b, C, c_bf16 != 0, N, K, num_splits, w, s)
+                          : launch_gemv_split<false>(a, b, C, c_bf16 != 0, N, K, num_splits, w, s);
+    }
+    return e == hipSuccess ? TA_OK : TA_ERR_LAUNCH;
+}
+
+ta_status gemv_split_workspace_bytes(int N, int num_splits, size_t *bytes)
+{
+    if (!bytes)
+        return TA_ERR_NULL_POINTER;
+    if (N < 1 || num_splits < 1 || num_splits > GV_MAX_SPLITS)
+        return TA_ERR_INVALID_SHAPE;
+    *bytes = num_splits > 1 ? (size_t)num_splits * N * 4 : 0;
+    return TA_OK;
+}
+
+// The split count whose workgroups fill their last round of CU slots most
+// evenly (one slot per CU per round; two 16-wave workgroups fit a CU), up
+// to two rounds, keeping at least 1024 rows per split; on a tie the fewer
+// workgroups.  Strips are 256 columns where N % 256 == 0, else 64; one
+// split runs the unsplit kernel, whose strips are 64 columns unless there
+// are 144 or more of 256, so with 256-column splits available it only
+// counts when that holds.  (Measured, the paper's V0-V7 shapes: a count
+// just past a multiple of 256 is 10-26 % slower than one just below it.)
+ta_status gemv_split_heuristic(int N, int K, int *num_splits)
+{
+    if (!num_splits)
+        return TA_ERR_NULL_POINTER;
+    if (N < 1 || K < 1)
+        return TA_ERR_INVALID_SHAPE;
+    constexpr int64_t CUS = 256;
+    const bool wide = N % 256 == 0;
+    const int64_t strips = wide ? N / 256 : ((int64_t)N + 63) / 64;
+    // is w1 workgroups' last round fuller than w2's
+    auto fuller = [](int64_t w1, int64_t w2) {
+        const int64_t r1 = CUS * ((w1 + CUS - 1) / CUS), r2 = CUS * ((w2 + CUS - 1) / CUS);
+        return w1 * r2 > w2 * r1;
+    };
+    int n = 1;
+    int64_t best = !wide || strips >= 144 ? strips : -1;
+    for (int sp = 2; sp <= GV_MAX_SPLITS && strips * sp <= 2 * CUS && K / sp >= 1024; ++sp)
+        if (best < 0 || fuller(strips * sp, best)) {
+            n = sp;
+            best = strips * sp;
+        }
+    *num_splits = n;
+    return TA_OK;
 }
 
 }  // extern "C"

@@ -62,6 +62,12 @@ def lib():
     L.mla_split_heuristic.argtypes = [i, i, i, i, ctypes.POINTER(i)]
     L.gemm_bf16.restype = i
     L.gemm_bf16.argtypes = [p, p, p, i, i, i, i, p]
+    L.gemv_bf16_split.restype = i
+    L.gemv_bf16_split.argtypes = [p, p, p, i, i, i, i, p, ctypes.c_size_t, p]
+    L.gemv_split_workspace_bytes.restype = i
+    L.gemv_split_workspace_bytes.argtypes = [i, i, ctypes.POINTER(ctypes.c_size_t)]
+    L.gemv_split_heuristic.restype = i
+    L.gemv_split_heuristic.argtypes = [i, i, ctypes.POINTER(i)]
     L.ssd_chunk_state.restype = i
     L.ssd_chunk_state.argtypes = [p, p, p, p, p] + [i] * 7 + [p]
     L.ssd_state_passing.restype = i
@@ -375,6 +381,71 @@ def gemm_bf16(a, b, out=None, out_dtype=None, stream=None):
     with _one_device(a, b, out):
         rc = gemm_bf16_raw(a.data_ptr(), b.data_ptr(), out.data_ptr(), dt == torch.bfloat16, M, N,
                            K, stream.cuda_stream)
+    if rc != TA_OK:
+        raise TileAttnError(rc, ta_status_string(rc))
+    return out
+
+
+def gemv_split_workspace_bytes(N: int, num_splits: int) -> int:
+    n = ctypes.c_size_t()
+    rc = lib().gemv_split_workspace_bytes(N, num_splits, ctypes.byref(n))
+    if rc != TA_OK:
+        raise TileAttnError(rc, ta_status_string(rc))
+    return n.value
+
+
+def gemv_split_heuristic(N: int, K: int) -> int:
+    n = ctypes.c_int()
+    rc = lib().gemv_split_heuristic(N, K, ctypes.byref(n))
+    if rc != TA_OK:
+        raise TileAttnError(rc, ta_status_string(rc))
+    return n.value
+
+
+def gemv_bf16_split_raw(A, B, C, c_bf16, N, K, num_splits, workspace, workspace_bytes,
+                        stream) -> int:
+    """gemv_bf16_split with integer pointers; returns the status code."""
+    return lib().gemv_bf16_split(A, B, C, int(bool(c_bf16)), N, K, int(num_splits), workspace,
+                                 int(workspace_bytes), stream)
+
+
+def gemv_bf16_split(a, b, num_splits: int | None = None, out=None, out_dtype=None,
+                    workspace=None, stream=None):
+    """C [1, N] = a [1, K] b [K, N] for contiguous bfloat16 GPU tensors, with
+    K split into ``num_splits`` ranges (default gemv_split_heuristic); C is
+    float32 (default) or bfloat16.  ``workspace`` (uint8 GPU tensor) is
+    allocated here if needed and not given; it must stay alive until the
+    launch has finished on ``stream``."""
+    import torch
+
+    for name, t in (("a", a), ("b", b)):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or t.dim() != 2 or not t.is_contiguous():
+            raise TypeError(f"{name} must be a contiguous 2-D bfloat16 GPU tensor")
+    M, K = a.shape
+    K2, N = b.shape
+    if M != 1 or K2 != K:
+        raise TileAttnError(2, f"inconsistent shapes a{tuple(a.shape)} b{tuple(b.shape)}")
+    dt = torch.float32 if out_dtype is None else out_dtype
+    if dt not in (torch.float32, torch.bfloat16):
+        raise TypeError("out_dtype must be torch.float32 or torch.bfloat16")
+    if num_splits is None:
+        num_splits = gemv_split_heuristic(N, K)
+    if out is None:
+        out = torch.empty((1, N), dtype=dt, device=a.device)
+    if out.dtype != dt or tuple(out.shape) != (1, N) or not out.is_contiguous():
+        raise TypeError(f"out must be a contiguous {dt} tensor of shape {(1, N)}")
+    need = gemv_split_workspace_bytes(N, num_splits)
+    if stream is None:
+        stream = torch.cuda.current_stream(a.device)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=a.device)
+        workspace.record_stream(stream)   # as in attn_fwd_split
+    if workspace.dtype != torch.uint8 or not workspace.is_cuda or not workspace.is_contiguous():
+        raise TypeError("workspace must be a contiguous uint8 GPU tensor")
+    with _one_device(a, b, out, workspace):
+        rc = gemv_bf16_split_raw(a.data_ptr(), b.data_ptr(), out.data_ptr(), dt == torch.bfloat16,
+                                 N, K, num_splits, workspace.data_ptr(), workspace.numel(),
+                                 stream.cuda_stream)
     if rc != TA_OK:
         raise TileAttnError(rc, ta_status_string(rc))
     return out

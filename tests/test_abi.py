@@ -267,6 +267,60 @@ def test_gemm_validation_before_any_hip_call(change, status):
     assert rc == status, f"{change}: got {ta.STATUS.get(rc, rc)}, want {ta.STATUS[status]}"
 
 
+# gemv_bf16_split: argument errors before any HIP call (fake pointers)
+GW = 0x60000000
+GEMV_OK = dict(A=GA, B=GB, C=GC, c_bf16=0, N=256, K=128, splits=2, ws=GW, ws_bytes=1 << 20,
+               stream=None)
+BAD_GEMV = [
+    (dict(A=0), 1), (dict(B=0), 1), (dict(C=0), 1),
+    (dict(N=0), 2), (dict(K=-8), 2), (dict(splits=0), 2), (dict(splits=65), 2),
+    (dict(N=96), 3), (dict(K=12), 3),
+    (dict(A=GA + 8), 4), (dict(B=GB + 2), 4), (dict(C=GC + 4), 4), (dict(ws=GW + 8), 4),
+    (dict(C=GA + 128), 6), (dict(C=GB + 1024), 6), (dict(c_bf16=1, C=GB + 128 * 256 * 2 - 16), 6),
+    (dict(ws=GA + 16), 6), (dict(ws=GB - 1024), 6), (dict(ws=GC - 2 * 256 * 4 + 16), 6),
+    (dict(ws=0), 8), (dict(ws_bytes=2 * 256 * 4 - 1), 8),
+]
+
+
+@no_gpu
+@pytest.mark.parametrize("change,status", BAD_GEMV, ids=[str(c) for c, _ in BAD_GEMV])
+def test_gemv_split_validation_before_any_hip_call(change, status):
+    a = dict(GEMV_OK, **change)
+    rc = ta.gemv_bf16_split_raw(a["A"], a["B"], a["C"], a["c_bf16"], a["N"], a["K"], a["splits"],
+                                a["ws"], a["ws_bytes"], a["stream"])
+    assert rc == status, f"{change}: got {ta.STATUS.get(rc, rc)}, want {ta.STATUS[status]}"
+
+
+def test_gemv_split_workspace_and_heuristic():
+    assert ta.gemv_split_workspace_bytes(9216, 7) == 7 * 9216 * 4
+    assert ta.gemv_split_workspace_bytes(9216, 1) == 0
+    for bad in [(0, 2), (64, 0), (64, 65)]:
+        with pytest.raises(ta.TileAttnError):
+            ta.gemv_split_workspace_bytes(*bad)
+    # the paper's V0-V7 (N, K): few 256-column strips split K, many do not
+    # (workgroups = 256-column strips x splits: 256, 504, 504, 224, 504, 252, 432, 252)
+    expect = {(16384, 16384): 4, (43008, 14336): 3, (14336, 14336): 9, (57344, 14336): 1,
+              (14336, 57344): 9, (9216, 9216): 7, (36864, 9216): 3, (9216, 36864): 7}
+    for (N, K), n in expect.items():
+        assert ta.gemv_split_heuristic(N, K) == n, (N, K)
+
+    def fill(w):   # share of the last round of 256 CU slots the workgroups fill
+        return w / (256 * -(-w // 256))
+
+    for N, K in [(64, 8), (64, 1 << 20), (320, 4096), (320, 1 << 20), (1024, 2048),
+                 (65536, 1024), (6400, 8192), (36864, 1 << 20), (256, 1 << 16)]:
+        n = ta.gemv_split_heuristic(N, K)
+        strips = N // 256 if N % 256 == 0 else -(-N // 64)
+        assert 1 <= n <= 64, (N, K, n)
+        if n > 1:
+            assert n * strips <= 512 and K // n >= 1024, (N, K, n)
+        # brute force: no allowed count fills the last round better
+        for m in range(2, 65):
+            if m * strips <= 512 and K // m >= 1024 and m != n:
+                assert fill(m * strips) <= fill(n * strips) + 1e-12 or (
+                    n == 1 and N % 256 == 0 and strips < 144), (N, K, n, m)
+
+
 # SSD chunk functions: argument errors before any HIP call (fake pointers).
 # Shapes: B=1, L=300, H=4, G=2 -> x 153600 B, Bm/Cm 153600 B, dt 4800 B,
 # cb 2 chunks x 2 groups x 256 KiB, states 2 x 4 x 32 KiB.

@@ -150,3 +150,66 @@ def test_gemv_bf16_out_and_deterministic(ta):
     assert torch.equal(c32.view(torch.int32), c32b.view(torch.int32))
     assert torch.equal(c16.view(torch.int16), c32.to(torch.bfloat16).view(torch.int16))
     check("gemv bf16 out", c16, a, b, bf16=True)
+
+
+# gemv_bf16_split: K split over workgroups, fp32 partial sums merged in order.
+# (N, K, splits): 256-column strips (N % 256 == 0) and 64-column ones, ranges
+# of uneven length, splits with fewer row groups than waves, more splits than
+# row groups (empty ranges), and the largest split count
+GEMV_SPLIT_SHAPES = [(256, 1024, 4), (320, 200, 3), (1024, 4096, 7), (64, 8, 5), (9216, 2056, 7),
+                     (2048, 3080, 64), (4096, 1000, 2), (36864, 1048, 3)]
+
+
+@pytest.mark.parametrize("shape", GEMV_SPLIT_SHAPES, ids=[str(s) for s in GEMV_SPLIT_SHAPES])
+def test_gemv_split_full_compare(ta, shape):
+    N, K, S = shape
+    print(f"gemv split N={N} K={K} splits={S}", flush=True)
+    a, b = gen.random_gemm_problem(1, N, K, seed=N + K + S)
+    c = torch.full((1, N), float("nan"), device="cuda")
+    # every workspace byte 0xFF (a NaN): a partial sum left unwritten shows
+    ws = torch.full((ta.gemv_split_workspace_bytes(N, S),), 255, dtype=torch.uint8, device="cuda")
+    ta.gemv_bf16_split(dev(a), dev(b), num_splits=S, out=c, workspace=ws)
+    torch.cuda.synchronize()
+    check(f"gemv split {shape}", c, a, b)
+
+
+@pytest.mark.parametrize("name", ["gemv_v7", "gemv_v5", "gemv_v0", "gemv_v6", "gemv_v1", "gemv_v2",
+                                  "gemv_v4"])
+def test_gemv_split_workload_sampled(ta, name):
+    """The matrix-vector shapes the split count heuristic splits, at full
+    size: every output finite, sampled columns against the oracle."""
+    w = gen.GEMM_WORKLOADS[name]
+    S = ta.gemv_split_heuristic(w.N, w.K)
+    print(f"gemv split workload {name} {w.describe()} splits={S}", flush=True)
+    assert S > 1
+    a, b = gen.make_gemm_inputs(w, seed=0)
+    c = torch.full((1, w.N), float("nan"), device="cuda")
+    ta.gemv_bf16_split(dev(a), dev(b), num_splits=S, out=c)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(c).all())
+    rng = np.random.default_rng(3)
+    cols = sorted({0, 1, 255, 256, w.N - 256, w.N - 1} | {int(x) for x in rng.integers(0, w.N, size=40)})
+    bs = np.ascontiguousarray(b[:, cols])
+    ref, scale = oracle.gemm(a, bs)[0], oracle.gemm_abs(a, bs)[0]
+    got = c[0, torch.tensor(cols)].cpu().numpy()
+    worst = float((np.abs(got - ref) / (REL_ABS * scale)).max())
+    print(f"{name} split: worst err/tol={worst:.3f}", flush=True)
+    assert worst <= 1.0
+
+
+def test_gemv_split_bf16_out_and_deterministic(ta):
+    """bf16 C is the fp32 result rounded once; repeated calls agree bit for
+    bit; one split is gemm_bf16's matrix-vector product, bit for bit."""
+    a, b = gen.random_gemm_problem(1, 2048, 6000, seed=12)
+    da, db = dev(a), dev(b)
+    c32 = ta.gemv_bf16_split(da, db, num_splits=5)
+    c32b = ta.gemv_bf16_split(da, db, num_splits=5)
+    c16 = ta.gemv_bf16_split(da, db, num_splits=5, out_dtype=torch.bfloat16)
+    c1 = ta.gemv_bf16_split(da, db, num_splits=1)
+    ref1 = ta.gemm_bf16(da, db)
+    torch.cuda.synchronize()
+    assert torch.equal(c32.view(torch.int32), c32b.view(torch.int32))
+    assert torch.equal(c16.view(torch.int16), c32.to(torch.bfloat16).view(torch.int16))
+    assert torch.equal(c1.view(torch.int32), ref1.view(torch.int32))
+    check("gemv split fp32", c32, a, b)
+    check("gemv split bf16 out", c16, a, b, bf16=True)
