@@ -529,19 +529,18 @@ __global__ __launch_bounds__(GV_COMBINE) void gemv_combine_kernel(const float *W
         return;
     const float *w = W + n;
     float sum = w[0];
-    int s = 1;
-    // eight rows' loads in flight before their adds
-    for (; s + 8 <= S; s += 8) {
+    // up to eight rows' loads in flight before their adds (the split counts
+    // in use are 2-9: one or two round trips instead of one per row)
+    for (int s = 1; s < S; s += 8) {
         float v[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
-            v[u] = w[(size_t)(s + u) * N];
+            v[u] = s + u < S ? w[(size_t)(s + u) * N] : 0.f;
 #pragma unroll
         for (int u = 0; u < 8; ++u)
-            sum += v[u];
+            if (s + u < S)
+                sum += v[u];
     }
-    for (; s < S; ++s)
-        sum += w[(size_t)s * N];
     if (CBF16)
         ((uint16_t *)C)[n] = (uint16_t)pack_bf16(sum, 0.f);
     else
