@@ -35,25 +35,45 @@ __device__ __forceinline__ u32x4s buffer_rsrc(const void *base, uint32_t bytes)
 // Lane l's 16 bytes at byte `voff` of the buffer land at LDS address
 // `lds` + 16 l (`lds` wave-uniform).  M0 is an operand of the statement, so
 // the compiler sets it (and keeps any value of its own) around the load.
+// NT: the load carries the non-temporal cache policy, for data that no other
+// workgroup reads again.
+template <bool NT = false>
 __device__ __forceinline__ void dma16(uint32_t lds, uint32_t voff, u32x4s rsrc)
 {
-    asm volatile("s_nop 0\n\t"   // one wait state between the M0 write and the load
-                 "buffer_load_dwordx4 %0, %1, 0 offen lds"
-                 :
-                 : "v"(voff), "s"(rsrc), "{m0}"(__builtin_amdgcn_readfirstlane(lds))
-                 : "memory");
+    if constexpr (NT)
+        asm volatile("s_nop 0\n\t"   // one wait state between the M0 write and the load
+                     "buffer_load_dwordx4 %0, %1, 0 offen nt lds"
+                     :
+                     : "v"(voff), "s"(rsrc), "{m0}"(__builtin_amdgcn_readfirstlane(lds))
+                     : "memory");
+    else
+        asm volatile("s_nop 0\n\t"
+                     "buffer_load_dwordx4 %0, %1, 0 offen lds"
+                     :
+                     : "v"(voff), "s"(rsrc), "{m0}"(__builtin_amdgcn_readfirstlane(lds))
+                     : "memory");
 }
 
 // The same with a wave-uniform byte offset `soff` (a scalar register) added to
 // the lane's `voff`.
+template <bool NT = false>
 __device__ __forceinline__ void dma16_soff(uint32_t lds, uint32_t voff, uint32_t soff,
                                            u32x4s rsrc)
 {
-    asm volatile("s_nop 0\n\t"
-                 "buffer_load_dwordx4 %0, %1, %2 offen lds"
-                 :
-                 : "v"(voff), "s"(rsrc), "s"(soff), "{m0}"(__builtin_amdgcn_readfirstlane(lds))
-                 : "memory");
+    if constexpr (NT)
+        asm volatile("s_nop 0\n\t"
+                     "buffer_load_dwordx4 %0, %1, %2 offen nt lds"
+                     :
+                     : "v"(voff), "s"(rsrc), "s"(soff),
+                       "{m0}"(__builtin_amdgcn_readfirstlane(lds))
+                     : "memory");
+    else
+        asm volatile("s_nop 0\n\t"
+                     "buffer_load_dwordx4 %0, %1, %2 offen lds"
+                     :
+                     : "v"(voff), "s"(rsrc), "s"(soff),
+                       "{m0}"(__builtin_amdgcn_readfirstlane(lds))
+                     : "memory");
 }
 
 __device__ __forceinline__ uint32_t lds_addr(const void *p)

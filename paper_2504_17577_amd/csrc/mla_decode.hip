@@ -204,7 +204,9 @@ struct Mla {
         va0 = row * (DL * 2) + 16 * (((hc & 3) >> 1) ^ lat_swz(row)) + 8 * (hc & 1);
     }
 
-    // DMA cache tile j (positions j*BN ..) into `stage`.  Each buffer
+    // DMA cache tile j (positions j*BN ..) into `stage`, with non-temporal
+    // loads: each tile is read by this workgroup only, once (measured 1-2.5 %
+    // faster on mla_b64_s8k and mla_b128_s4k, the same output).  Each buffer
     // resource starts at the tile and ends after its last valid row; a row
     // past Skv re-reads the last valid row (its scores are masked and its
     // weights zero), so no lane addresses outside the cache.
@@ -219,7 +221,7 @@ struct Mla {
         if (valid == BN) {
 #pragma unroll
             for (int i = 0; i < LAT_PER_THREAD; ++i)
-                tileattn_dma::dma16_soff(lat_base + i * NT * 16, lat_off[i & 1],
+                tileattn_dma::dma16_soff<true>(lat_base + i * NT * 16, lat_off[i & 1],
                                          16 * (i >> 1) * lat_pitch, rl);
         } else {
             const int last = valid - 1;
@@ -231,7 +233,7 @@ struct Mla {
                 const int src = row > last ? last : row;
                 const uint32_t o = lat_off[i & 1] + (uint32_t)((src - 8 * (i & 1) - wave_u) *
                                                                (int)lat_pitch);
-                tileattn_dma::dma16(lat_base + i * NT * 16, o, rl);
+                tileattn_dma::dma16<true>(lat_base + i * NT * 16, o, rl);
             }
         }
         if (rot_wave) {
@@ -240,7 +242,7 @@ struct Mla {
             // row 8w + l/8 is lane-dependent: clamp per lane
             const int row = 8 * (wave_u & 3) + lane / 8;
             const int shift = row > valid - 1 ? row - (valid - 1) : 0;
-            tileattn_dma::dma16(tileattn_dma::lds_addr(stage + LAT_BYTES) + wave_u * 64 * 16,
+            tileattn_dma::dma16<true>(tileattn_dma::lds_addr(stage + LAT_BYTES) + wave_u * 64 * 16,
                                 rot_off - (uint32_t)shift * rot_pitch, rr);
         }
     }
